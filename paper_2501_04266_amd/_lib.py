@@ -1,0 +1,140 @@
+"""ctypes binding of libzq.so (include/zq.h).
+
+Argument marshalling only: every step runs in the HIP kernels.  Tensors are
+torch tensors on the GPU (torch is used for device memory and streams); the
+work is enqueued on torch's current stream unless `stream` is given.  There is
+no CPU fallback: if the library is not built this module raises on use.
+"""
+import ctypes
+import os
+
+import torch  # noqa: F401  -- loads torch's HIP runtime first, so libzq binds to the same one
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libzq.so")
+
+ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
+STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",
+          -5: "ZQ_E_SIZE", -6: "ZQ_E_P", -7: "ZQ_E_HIP", -8: "ZQ_E_ALIAS"}
+EXPORTS = ["qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
+           "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
+
+_TORCH_DT = {torch.float32: ZQ_F32, torch.float16: ZQ_F16, torch.bfloat16: ZQ_BF16}
+_DT_TORCH = {v: k for k, v in _TORCH_DT.items()}
+_lib = None
+
+
+class ZQError(RuntimeError):
+    def __init__(self, status, what):
+        self.status = status
+        super().__init__(f"{what}: {STATUS.get(status, status)} ({lib().zq_status_string(status).decode()})")
+
+
+def lib():
+    """The loaded libzq.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2501_04266_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i64, i32, ci = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int
+    sig = {
+        "qwz_quantize": [vp, ci, i64, i32, vp, vp, vp],
+        "qwz_dequantize": [vp, vp, i64, i32, vp, ci, vp],
+        "qgz_quantize": [vp, ci, i64, i32, vp, vp, vp],
+        "qgz_dequantize": [vp, vp, i64, i32, vp, ci, vp],
+        "qgz_reduce_level": [vp, vp, i32, i64, i32, vp, vp, vp],
+    }
+    for name, args in sig.items():
+        fn = getattr(L, name)
+        fn.argtypes, fn.restype = args, ci
+    L.zq_num_scales.argtypes, L.zq_num_scales.restype = [i64, i32], i64
+    L.zq_int4_bytes.argtypes, L.zq_int4_bytes.restype = [i64], i64
+    L.zq_status_string.argtypes, L.zq_status_string.restype = [ci], ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def num_scales(n, block):
+    return (n + block - 1) // block
+
+
+def int4_bytes(n):
+    return (n + 1) // 2
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _dev(t, name):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _check(status, what):
+    if status != 0:
+        raise ZQError(status, what)
+
+
+def qwz_quantize(x, block=256, codes=None, scales=None, stream=None):
+    """INT8 block quantisation of x (f32/f16/bf16) -> (codes int8[n], scales f32[ceil(n/B)])."""
+    n = x.numel()
+    if codes is None:
+        codes = torch.empty(n, dtype=torch.int8, device=x.device)
+    if scales is None:
+        scales = torch.empty(num_scales(n, block), dtype=torch.float32, device=x.device)
+    _check(lib().qwz_quantize(_dev(x, "x"), _TORCH_DT[x.dtype], n, block, _dev(codes, "codes"),
+                              _dev(scales, "scales"), _stream(stream)), "qwz_quantize")
+    return codes, scales
+
+
+def qwz_dequantize(codes, scales, block=256, out_dtype=torch.bfloat16, y=None, n=None, stream=None):
+    n = codes.numel() if n is None else n
+    if y is None:
+        y = torch.empty(n, dtype=out_dtype, device=codes.device)
+    _check(lib().qwz_dequantize(_dev(codes, "codes"), _dev(scales, "scales"), n, block, _dev(y, "y"),
+                                _TORCH_DT[y.dtype], _stream(stream)), "qwz_dequantize")
+    return y
+
+
+def qgz_quantize(g, block=128, packed=None, scales=None, stream=None):
+    """INT4 block quantisation -> (packed uint8[ceil(n/2)], scales f32[ceil(n/B)])."""
+    n = g.numel()
+    if packed is None:
+        packed = torch.empty(int4_bytes(n), dtype=torch.uint8, device=g.device)
+    if scales is None:
+        scales = torch.empty(num_scales(n, block), dtype=torch.float32, device=g.device)
+    _check(lib().qgz_quantize(_dev(g, "g"), _TORCH_DT[g.dtype], n, block, _dev(packed, "packed"),
+                              _dev(scales, "scales"), _stream(stream)), "qgz_quantize")
+    return packed, scales
+
+
+def qgz_dequantize(packed, scales, n, block=128, out_dtype=torch.float32, y=None, stream=None):
+    if y is None:
+        y = torch.empty(n, dtype=out_dtype, device=packed.device)
+    _check(lib().qgz_dequantize(_dev(packed, "packed"), _dev(scales, "scales"), n, block, _dev(y, "y"),
+                                _TORCH_DT[y.dtype], _stream(stream)), "qgz_dequantize")
+    return y
+
+
+def qgz_reduce_level(packed_in, scales_in, P, m, block=128, packed_out=None, scales_out=None, stream=None):
+    """Dequant -> sum over P slices (ascending) -> INT4 requant.  packed_in holds
+    P slices of ceil(m/2) bytes back to back, scales_in P x ceil(m/B)."""
+    dev = packed_in.device
+    if packed_out is None:
+        packed_out = torch.empty(int4_bytes(m), dtype=torch.uint8, device=dev)
+    if scales_out is None:
+        scales_out = torch.empty(num_scales(m, block), dtype=torch.float32, device=dev)
+    if packed_in.numel() < P * int4_bytes(m) or scales_in.numel() < P * num_scales(m, block):
+        raise ValueError("slice buffers smaller than P slices of m elements")
+    _check(lib().qgz_reduce_level(_dev(packed_in, "packed_in"), _dev(scales_in, "scales_in"), P, m, block,
+                                  _dev(packed_out, "packed_out"), _dev(scales_out, "scales_out"),
+                                  _stream(stream)), "qgz_reduce_level")
+    return packed_out, scales_out

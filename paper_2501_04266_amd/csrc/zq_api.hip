@@ -1,0 +1,221 @@
+// zq_api.hip -- the C ABI declared in include/zq.h: argument validation on
+// the host, grid sizing, and launches on the caller's stream.
+//
+// Every check runs before anything is enqueued, so an argument error writes
+// no output byte.  The library allocates nothing and keeps no per-call state;
+// the only process-wide value is the optional workgroup cap read once from
+// ZQ_MAX_WORKGROUPS (used to vary launch geometry in determinism tests).
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stdlib.h>
+
+#include <tuple>
+#include <utility>
+
+#include "zq.h"
+#include "zq_internal.h"
+
+namespace {
+
+using namespace zq;
+
+int max_workgroups() {
+  static const int cap = [] {
+    const char* e = getenv("ZQ_MAX_WORKGROUPS");
+    long v = e ? strtol(e, nullptr, 10) : 0;
+    return (v >= 1 && v <= (1L << 30)) ? (int)v : 8192;
+  }();
+  return cap;
+}
+
+unsigned grid_for(int64_t units, int64_t units_per_wg) {
+  int64_t g = (units + units_per_wg - 1) / units_per_wg;
+  if (g < 1) g = 1;
+  if (g > max_workgroups()) g = max_workgroups();
+  return (unsigned)g;
+}
+
+// Launch with the kernel's exact parameter types; returns ZQ_E_HIP when the
+// runtime rejects the launch.
+template <typename... KArgs, typename... Args>
+int launch(void (*kern)(KArgs...), unsigned grid, unsigned block, hipStream_t st, Args&&... args) {
+  std::tuple<KArgs...> tup(std::forward<Args>(args)...);
+  void* argv[sizeof...(KArgs)];
+  std::apply([&](auto&... a) {
+    int i = 0;
+    ((argv[i++] = static_cast<void*>(&a)), ...);
+  }, tup);
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3(grid), dim3(block), argv, 0, st);
+  return e == hipSuccess ? ZQ_OK : ZQ_E_HIP;
+}
+
+int log2_block(int32_t block) {
+  if (block < 32 || block > 1024 || (block & (block - 1)) != 0) return -1;
+  int lg = 0;
+  while ((1 << lg) < block) ++lg;
+  return lg;
+}
+
+bool dtype_ok(int dt) { return dt == ZQ_F32 || dt == ZQ_F16 || dt == ZQ_BF16; }
+int64_t elem_bytes(int dt) { return dt == ZQ_F32 ? 4 : 2; }
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+struct Range {
+  const void* p;
+  int64_t bytes;
+};
+bool overlap(Range a, Range b) {
+  uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
+  return a0 < b0 + (uintptr_t)b.bytes && b0 < a0 + (uintptr_t)a.bytes;
+}
+bool any_overlap(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
+  for (const Range& o : outs) {
+    for (const Range& i : ins)
+      if (overlap(o, i)) return true;
+  }
+  // outputs must not overlap each other either
+  for (auto o1 = outs.begin(); o1 != outs.end(); ++o1)
+    for (auto o2 = o1 + 1; o2 != outs.end(); ++o2)
+      if (overlap(*o1, *o2)) return true;
+  return false;
+}
+
+int64_t num_scales(int64_t n, int32_t block) { return (n + block - 1) / block; }
+
+// Shared body of qwz_quantize / qgz_quantize.
+int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, float* scales, void* stream,
+             int qbits) {
+  if (n < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (!dtype_ok(xt)) return ZQ_E_DTYPE;
+  if (n == 0) return ZQ_OK;
+  if (!x || !out || !scales) return ZQ_E_NULL;
+  if (!aligned(x, 16) || !aligned(out, 16) || !aligned(scales, 4)) return ZQ_E_ALIGN;
+  const int64_t nb = num_scales(n, block);
+  const int64_t out_bytes = qbits == 8 ? n : (n + 1) / 2;
+  if (any_overlap({{out, out_bytes}, {scales, 4 * nb}}, {{x, n * elem_bytes(xt)}})) return ZQ_E_ALIAS;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t nfull = n / block;
+  int rc = ZQ_OK;
+  if (nfull > 0) {
+    const int64_t blocks_per_wave = 1024 / block;  // 64 lanes x 16 elements
+    const int64_t waves = (nfull + blocks_per_wave - 1) / blocks_per_wave;
+    rc = launch(quant_kernel(xt, qbits, lgB), grid_for(waves, kThreads / 64), kThreads, st, x, nfull, out, scales);
+    if (rc != ZQ_OK) return rc;
+  }
+  const int64_t rest = n - nfull * block;
+  if (rest > 0) {
+    rc = launch(quant_tail_kernel(xt, qbits), 1u, 64u, st, x, nfull * (int64_t)block, (int)rest, out,
+                scales + nfull);
+  }
+  return rc;
+}
+
+int dequantize(const void* codes, const float* scales, int64_t n, int32_t block, void* y, int yt, void* stream,
+               int qbits) {
+  if (n < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (!dtype_ok(yt)) return ZQ_E_DTYPE;
+  if (n == 0) return ZQ_OK;
+  if (!codes || !scales || !y) return ZQ_E_NULL;
+  if (!aligned(codes, 16) || !aligned(y, 16) || !aligned(scales, 4)) return ZQ_E_ALIGN;
+  const int64_t nb = num_scales(n, block);
+  const int64_t in_bytes = qbits == 8 ? n : (n + 1) / 2;
+  if (any_overlap({{y, n * elem_bytes(yt)}}, {{codes, in_bytes}, {scales, 4 * nb}})) return ZQ_E_ALIAS;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const unsigned grid = grid_for(n >> 4, kThreads);
+  if (qbits == 8)
+    return launch(dequant8_kernel(yt), grid, kThreads, st, static_cast<const int8_t*>(codes), scales, n, lgB, y);
+  return launch(dequant4_kernel(yt), grid, kThreads, st, static_cast<const uint8_t*>(codes), scales, n, lgB, y);
+}
+
+}  // namespace
+
+extern "C" {
+
+int qwz_quantize(const void* x, zq_dtype xt, int64_t n, int32_t block, int8_t* codes, float* scales,
+                 void* stream) {
+  return quantize(x, xt, n, block, reinterpret_cast<uint8_t*>(codes), scales, stream, 8);
+}
+
+int qwz_dequantize(const int8_t* codes, const float* scales, int64_t n, int32_t block, void* y, zq_dtype yt,
+                   void* stream) {
+  return dequantize(codes, scales, n, block, y, yt, stream, 8);
+}
+
+int qgz_quantize(const void* g, zq_dtype gt, int64_t n, int32_t block, uint8_t* packed, float* scales,
+                 void* stream) {
+  return quantize(g, gt, n, block, packed, scales, stream, 4);
+}
+
+int qgz_dequantize(const uint8_t* packed, const float* scales, int64_t n, int32_t block, void* y, zq_dtype yt,
+                   void* stream) {
+  return dequantize(packed, scales, n, block, y, yt, stream, 4);
+}
+
+int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
+                     uint8_t* packed_out, float* scales_out, void* stream) {
+  if (m < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (P < 1 || P > 1024) return ZQ_E_P;
+  if (m == 0) return ZQ_OK;
+  if (!packed_in || !scales_in || !packed_out || !scales_out) return ZQ_E_NULL;
+  if (!aligned(packed_in, 16) || !aligned(packed_out, 16) || !aligned(scales_in, 4) || !aligned(scales_out, 4))
+    return ZQ_E_ALIGN;
+  const int64_t slice_bytes = (m + 1) / 2, nb = num_scales(m, block);
+  if (any_overlap({{packed_out, slice_bytes}, {scales_out, 4 * nb}},
+                  {{packed_in, slice_bytes * P}, {scales_in, 4 * nb * P}}))
+    return ZQ_E_ALIAS;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int64_t generic_from = 0;
+  if (m % 32 == 0) {
+    // every slice starts 16-byte aligned: vector path over the full blocks
+    const int64_t nfull = m / block;
+    if (nfull > 0) {
+      const int64_t waves = (nfull * block + 2047) / 2048;  // 64 lanes x 32 elements
+      int rc = launch(reduce_kernel(lgB), grid_for(waves, kThreads / 64), kThreads, st, packed_in, scales_in, (int)P,
+                      slice_bytes, nb, nfull, packed_out, scales_out);
+      if (rc != ZQ_OK) return rc;
+    }
+    generic_from = nfull;
+  }
+  // remaining blocks (a short last block, or all of them when slices are not
+  // 16-byte aligned): one wave per block
+  for (int64_t b0 = generic_from; b0 < nb; b0 += (1LL << 30)) {
+    const int64_t cnt = (nb - b0) < (1LL << 30) ? (nb - b0) : (1LL << 30);
+    int rc = launch(reduce_generic_kernel(), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes, nb, m,
+                    (int)block, b0, packed_out, scales_out);
+    if (rc != ZQ_OK) return rc;
+  }
+  return ZQ_OK;
+}
+
+int64_t zq_num_scales(int64_t n, int32_t block) {
+  if (n < 0 || log2_block(block) < 0) return -1;
+  return num_scales(n, block);
+}
+
+int64_t zq_int4_bytes(int64_t n) { return n < 0 ? -1 : (n + 1) / 2; }
+
+const char* zq_status_string(int status) {
+  switch (status) {
+    case ZQ_OK: return "ok";
+    case ZQ_E_NULL: return "null pointer";
+    case ZQ_E_BLOCK: return "block must be a power of two in [32, 1024]";
+    case ZQ_E_DTYPE: return "unknown dtype";
+    case ZQ_E_ALIGN: return "misaligned pointer (elements/codes 16 B, scales 4 B)";
+    case ZQ_E_SIZE: return "negative size";
+    case ZQ_E_P: return "slice count outside [1, 1024]";
+    case ZQ_E_HIP: return "HIP launch failed";
+    case ZQ_E_ALIAS: return "an output overlaps an input";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

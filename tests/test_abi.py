@@ -1,0 +1,112 @@
+"""CPU tests of the C ABI boundary (no kernel is launched).
+
+The library must load and export every function include/zq.h declares; the
+host-only helpers and every argument check (which runs before anything is
+enqueued) are exercised with fake device pointers.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "zq.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", src, re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2501_04266_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2501_04266_amd import build
+        build.build()
+    return _lib.lib()
+
+
+def test_header_declares_the_five_calls():
+    names = _declared()
+    for fn in ("qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
+               "zq_num_scales", "zq_int4_bytes", "zq_status_string"):
+        assert fn in names, fn
+
+
+def test_every_declared_symbol_is_exported(L):
+    for fn in _declared():
+        assert hasattr(L, fn), f"libzq.so does not export {fn}"
+
+
+def test_binding_names_match_header():
+    from paper_2501_04266_amd import _lib
+    assert sorted(_lib.EXPORTS) == _declared()
+
+
+def test_size_helpers(L):
+    assert L.zq_num_scales(0, 256) == 0
+    assert L.zq_num_scales(1, 256) == 1
+    assert L.zq_num_scales(123_456_789, 256) == 482_254
+    assert L.zq_num_scales(123_456_789, 64) == 1_929_013
+    assert L.zq_num_scales(10, 48) == -1
+    assert L.zq_num_scales(-1, 64) == -1
+    assert L.zq_int4_bytes(123_456_789) == 61_728_395
+    assert L.zq_int4_bytes(-3) == -1
+    for st in range(-8, 1):
+        assert L.zq_status_string(st)
+    assert L.zq_status_string(-99) == b"unknown status"
+
+
+# fake, suitably aligned "device" addresses: validation never dereferences them
+A = 0x7F0000000000
+B = 0x7F0010000000
+C = 0x7F0020000000
+
+
+@pytest.mark.parametrize("call,args,status", [
+    ("qwz_quantize", (A, 0, -1, 256, B, C, None), -5),
+    ("qwz_quantize", (A, 0, 100, 48, B, C, None), -2),
+    ("qwz_quantize", (A, 0, 100, 16, B, C, None), -2),
+    ("qwz_quantize", (A, 0, 100, 2048, B, C, None), -2),
+    ("qwz_quantize", (A, 7, 100, 256, B, C, None), -3),
+    ("qwz_quantize", (None, 0, 100, 256, B, C, None), -1),
+    ("qwz_quantize", (A, 0, 100, 256, None, C, None), -1),
+    ("qwz_quantize", (A + 4, 0, 100, 256, B, C, None), -4),
+    ("qwz_quantize", (A, 0, 100, 256, B + 8, C, None), -4),
+    ("qwz_quantize", (A, 0, 100, 256, B, C + 2, None), -4),
+    ("qwz_quantize", (A, 0, 100, 256, A + 256, C, None), -8),
+    ("qwz_quantize", (A, 0, 100, 256, B, A + 396, None), -8),
+    ("qwz_quantize", (A, 0, 0, 256, None, None, None), 0),
+    ("qwz_dequantize", (A, C, 100, 256, A + 96, 2, None), -8),
+    ("qwz_dequantize", (A, C, 100, 256, B, 3, None), -3),
+    ("qwz_dequantize", (A, None, 100, 256, B, 2, None), -1),
+    ("qwz_dequantize", (A, C, 0, 256, B, 2, None), 0),
+    # packed output of 100 elements is 50 bytes: scales at +48 overlap it
+    ("qgz_quantize", (A, 0, 100, 64, B, B + 48, None), -8),
+    # bf16 input of 1001 elements spans 2002 bytes: output at +2000 overlaps it
+    ("qgz_quantize", (A, 2, 1001, 64, A + 2000, C, None), -8),
+    ("qgz_dequantize", (A, C, 1001, 64, B + 4, 0, None), -4),
+])
+def test_argument_errors(L, call, args, status):
+    conv = [ctypes.c_void_p(a) if isinstance(a, int) and a > 1 << 20 else a for a in args]
+    got = getattr(L, call)(*conv)
+    assert got == status, f"{call}{args}: got {got}, want {status}"
+
+
+def test_reduce_argument_errors(L):
+    f = L.qgz_reduce_level
+    vp = ctypes.c_void_p
+    assert f(vp(A), vp(C), 0, 256, 128, vp(B), vp(B + 4096), None) == -6
+    assert f(vp(A), vp(C), 1025, 256, 128, vp(B), vp(B + 4096), None) == -6
+    assert f(vp(A), vp(C), 8, -1, 128, vp(B), vp(B + 4096), None) == -5
+    assert f(vp(A), vp(C), 8, 256, 100, vp(B), vp(B + 4096), None) == -2
+    assert f(vp(A), vp(C), 8, 0, 128, None, None, None) == 0
+    assert f(vp(A), None, 8, 256, 128, vp(B), vp(B + 4096), None) == -1
+    assert f(vp(A + 8), vp(C), 8, 256, 128, vp(B), vp(B + 4096), None) == -4
+    # output overlapping slice 3 of the input
+    assert f(vp(A), vp(C), 8, 256, 128, vp(A + 3 * 128), vp(B + 4096), None) == -8
+    # output scales overlapping input scales
+    assert f(vp(A), vp(C), 8, 256, 128, vp(B), vp(C + 8), None) == -8

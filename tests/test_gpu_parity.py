@@ -1,0 +1,246 @@
+"""GPU parity: every HIP entry point, called through the C ABI, against the
+CPU oracle on the same seeded host inputs.  Bit-exact on codes, packed bytes,
+scales and dequantised outputs (fp32 / bf16 / fp16 bit patterns).
+
+Sizes span several wave tiles and ragged tails (n not a multiple of the
+block, odd n for INT4, slices that are not 16-byte aligned), every block
+size, every element dtype, and the degenerate inputs of the method (zero and
+sub-threshold blocks, exact ties, elements at code midpoints, outliers).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_04266_amd as zq
+from tests import pin_checks as pc
+from tests.gpu_util import assert_bits_equal, from_dev, to_dev
+
+pytestmark = pytest.mark.gpu
+
+KINDS = ["normal", "outlier", "zeros", "tiny", "ties", "const"]
+
+
+def _input(n, kind, seed, dtype):
+    x32 = pc._tiny_inputs(seed, n, kind) if n else np.zeros(0, np.float32)
+    return pc._as_dtype(x32, dtype)
+
+
+def _run_quant(op, x_np, dtype, block):
+    x = to_dev(x_np, dtype)
+    if op == "qwz":
+        c, s = zq.qwz_quantize(x, block)
+    else:
+        c, s = zq.qgz_quantize(x, block)
+    torch.cuda.synchronize()
+    return from_dev(c), from_dev(s)
+
+
+def _oracle_quant(op, x_np, dtype, block):
+    return (oracle.qwz_quantize if op == "qwz" else oracle.qgz_quantize)(x_np, block, dtype)
+
+
+QUANT_CASES = []
+for op in ("qwz", "qgz"):
+    for dtype in ("f32", "bf16", "f16"):
+        for block in (32, 64, 128, 256, 512, 1024):
+            for n in (1, 17, 1024 * 3 + 5, 65536 + 1021):
+                QUANT_CASES.append((op, dtype, block, n))
+
+
+@pytest.mark.parametrize("op,dtype,block,n", QUANT_CASES)
+def test_quantize_parity(op, dtype, block, n):
+    for i, kind in enumerate(KINDS):
+        x = _input(n, kind, 1000 * block + n + i, dtype)
+        gc, gs = _run_quant(op, x, dtype, block)
+        oc, os_ = _oracle_quant(op, x, dtype, block)
+        assert_bits_equal(gc, oc, f"{op} codes {dtype} B={block} n={n} {kind}", block if op == "qwz" else block // 2)
+        assert_bits_equal(gs, os_, f"{op} scales {dtype} B={block} n={n} {kind}")
+
+
+@pytest.mark.parametrize("op,block", [("qwz", 256), ("qgz", 128), ("qgz", 64), ("qwz", 32)])
+def test_quantize_midpoints(op, block):
+    qmax = 127 if op == "qwz" else 7
+    xs = [pc.midpoint_block(qmax, block, 60 + k)[0] for k in range(6)]
+    x = np.concatenate(xs)
+    gc, gs = _run_quant(op, x, "f32", block)
+    oc, os_ = _oracle_quant(op, x, "f32", block)
+    assert_bits_equal(gc, oc, f"{op} midpoint codes")
+    assert_bits_equal(gs, os_, f"{op} midpoint scales")
+
+
+def test_quantize_large_ragged():
+    g = np.random.default_rng(5)
+    n = (1 << 22) + 777
+    x = (g.standard_normal(n) * 0.02).astype(np.float32)
+    x[g.choice(n, n // 1000, replace=False)] *= 100
+    for op, block in (("qwz", 256), ("qgz", 128), ("qgz", 64)):
+        gc, gs = _run_quant(op, x, "f32", block)
+        oc, os_ = _oracle_quant(op, x, "f32", block)
+        assert_bits_equal(gc, oc, f"{op} codes large")
+        assert_bits_equal(gs, os_, f"{op} scales large")
+
+
+DEQ_CASES = []
+for op in ("qwz", "qgz"):
+    for out in ("f32", "bf16", "f16"):
+        for block in (32, 128, 256, 1024):
+            for n in (1, 15, 16, 33, 4096 * 3 + 7, 65536 + 1021):
+                DEQ_CASES.append((op, out, block, n))
+
+
+@pytest.mark.parametrize("op,out,block,n", DEQ_CASES)
+def test_dequantize_parity(op, out, block, n):
+    for i, kind in enumerate(("normal", "outlier", "tiny", "zeros")):
+        x = _input(n, kind, 7000 + n + block + i, "f32")
+        if op == "qwz":
+            c, s = oracle.qwz_quantize(x, block)
+            want = oracle.qwz_dequantize(c, s, block, out)
+            y = zq.qwz_dequantize(to_dev(c), to_dev(s), block, out_dtype={"f32": torch.float32, "bf16": torch.bfloat16,
+                                                                           "f16": torch.float16}[out])
+        else:
+            c, s = oracle.qgz_quantize(x, block)
+            want = oracle.qgz_dequantize(c, s, n, block, out)
+            y = zq.qgz_dequantize(to_dev(c), to_dev(s), n, block, out_dtype={"f32": torch.float32,
+                                                                              "bf16": torch.bfloat16,
+                                                                              "f16": torch.float16}[out])
+        torch.cuda.synchronize()
+        assert_bits_equal(from_dev(y), want, f"{op} dequant -> {out} B={block} n={n} {kind}")
+
+
+def test_dequantize_golden_rounding():
+    """Output narrowing ties (bf16 and f16 subnormal) on the GPU."""
+    c = np.array([1, 3, -1, 127] + [0] * 252, np.int8)
+    s = np.array([1.00390625], np.float32)
+    y = zq.qwz_dequantize(to_dev(c), to_dev(s), 256, out_dtype=torch.bfloat16)
+    assert_bits_equal(from_dev(y), oracle.qwz_dequantize(c, s, 256, "bf16"), "bf16 ties")
+    nib = np.array([1, 3, -1, 0] + [0] * 28, np.int64) & 0xF
+    packed = (nib[0::2] | (nib[1::2] << 4)).astype(np.uint8)
+    s = np.array([2.0 ** -25], np.float32)
+    y = zq.qgz_dequantize(to_dev(packed), to_dev(s), 32, 32, out_dtype=torch.float16)
+    assert_bits_equal(from_dev(y), oracle.qgz_dequantize(packed, s, 32, 32, "f16"), "f16 subnormal ties")
+
+
+def _slices(P, m, block, seed, scale_spread=True):
+    g = np.random.default_rng(seed)
+    xs = []
+    for p in range(P):
+        sd = 10.0 ** g.uniform(-4, 0) if scale_spread else 1e-3
+        x = (g.standard_normal(m) * sd).astype(np.float32)
+        if m > 4 * block:
+            x[block:2 * block] = 0.0          # a zero block in every slice
+        xs.append(x)
+    q = [oracle.qgz_quantize(x, block) for x in xs]
+    return np.concatenate([a for a, _ in q]), np.concatenate([b for _, b in q])
+
+
+REDUCE_CASES = []
+for P in (1, 2, 3, 4, 8, 48):
+    for block in (32, 64, 128, 256, 1024):
+        for m in (32, 2048 * 3 + block, 65536 + 128):
+            REDUCE_CASES.append((P, block, m))
+# ragged m: not a multiple of the block, of 32, odd
+for P, block, m in ((2, 128, 1000), (3, 64, 999), (8, 128, 65536 + 77), (48, 64, 4095), (5, 1024, 3000),
+                    (4, 32, 33), (2, 256, 1)):
+    REDUCE_CASES.append((P, block, m))
+
+
+@pytest.mark.parametrize("P,block,m", REDUCE_CASES)
+def test_reduce_level_parity(P, block, m):
+    pin, sin = _slices(P, m, block, 31 * P + m + block)
+    po, so = oracle.qgz_reduce_level(pin, sin, P, m, block)
+    gp, gs = zq.qgz_reduce_level(to_dev(pin), to_dev(sin), P, m, block)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(gp), po, f"reduce packed P={P} B={block} m={m}", block // 2)
+    assert_bits_equal(from_dev(gs), so, f"reduce scales P={P} B={block} m={m}")
+
+
+def test_reduce_identical_and_cancelling():
+    m, block = 8192, 128
+    g = np.random.default_rng(8)
+    x = (g.standard_normal(m) * 1e-3).astype(np.float32)
+    p0, s0 = oracle.qgz_quantize(x, block)
+    for P in (2, 8, 48):
+        gp, gs = zq.qgz_reduce_level(to_dev(np.tile(p0, P)), to_dev(np.tile(s0, P)), P, m, block)
+        po, so = oracle.qgz_reduce_level(np.tile(p0, P), np.tile(s0, P), P, m, block)
+        torch.cuda.synchronize()
+        assert_bits_equal(from_dev(gp), po, f"identical P={P}")
+        assert_bits_equal(from_dev(gs), so, f"identical P={P} scales")
+    pn, sn = oracle.qgz_quantize(-x, block)
+    gp, gs = zq.qgz_reduce_level(to_dev(np.concatenate([p0, pn])), to_dev(np.concatenate([s0, sn])), 2, m, block)
+    torch.cuda.synchronize()
+    assert not from_dev(gp).any() and not from_dev(gs).any()
+
+
+def test_three_level_chain_small():
+    """The hierarchical chain (fan-ins 2, 4, 48) at a reduced size, composed
+    from the C ABI calls, against the oracle's chain."""
+    block, fanins, rank = 128, [2, 4, 48], 0
+    n = 2 * 4 * 48 * block * 4
+    g = np.random.default_rng(12)
+    own = (g.standard_normal(n) * 1e-3).astype(np.float32)
+    peers, m = [], n
+    for k, P in enumerate(fanins):
+        m //= P
+        lvl = []
+        for p in range(P):
+            xs = (np.random.default_rng([4, 2, k, p]).standard_normal(m) * 1e-3).astype(np.float32)
+            lvl.append(oracle.qgz_quantize(xs, block) if p != rank else None)
+        peers.append(lvl)
+    op_, os_ = oracle.qgz_quantize(own, block)
+    outs = oracle.chain(op_, os_, n, fanins, peers, rank, block)
+    want = oracle.qgz_dequantize(outs[-1][0], outs[-1][1], outs[-1][2], block, "f32")
+
+    gp, gs = zq.qgz_quantize(to_dev(own), block)
+    cur_m = n
+    for k, P in enumerate(fanins):
+        m = cur_m // P
+        mb, nbm = (m + 1) // 2, m // block
+        pin = torch.empty(P * mb, dtype=torch.uint8, device="cuda")
+        sin = torch.empty(P * nbm, dtype=torch.float32, device="cuda")
+        for p in range(P):
+            if p == rank:
+                pin[p * mb:(p + 1) * mb] = gp[rank * mb:(rank + 1) * mb]
+                sin[p * nbm:(p + 1) * nbm] = gs[rank * nbm:(rank + 1) * nbm]
+            else:
+                pin[p * mb:(p + 1) * mb] = to_dev(peers[k][p][0])
+                sin[p * nbm:(p + 1) * nbm] = to_dev(peers[k][p][1])
+        gp, gs = zq.qgz_reduce_level(pin, sin, P, m, block)
+        torch.cuda.synchronize()
+        assert_bits_equal(from_dev(gp), outs[k][0], f"chain level {k} packed")
+        assert_bits_equal(from_dev(gs), outs[k][1], f"chain level {k} scales")
+        cur_m = m
+    y = zq.qgz_dequantize(gp, gs, cur_m, block, out_dtype=torch.float32)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(y), want, "chain final dequant")
+
+
+def test_empty_is_noop():
+    x = torch.empty(0, device="cuda")
+    c, s = zq.qwz_quantize(x, 256)
+    assert c.numel() == 0 and s.numel() == 0
+
+
+def test_async_on_side_stream():
+    """Work goes to the given stream; results are complete after syncing it."""
+    g = np.random.default_rng(2)
+    x = (g.standard_normal(1 << 20) * 1e-3).astype(np.float32)
+    want = oracle.qgz_quantize(x, 128)
+    s = torch.cuda.Stream()
+    xd = to_dev(x)
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        gp, gs = zq.qgz_quantize(xd, 128)
+    s.synchronize()
+    assert_bits_equal(from_dev(gp), want[0], "side stream packed")
+    assert_bits_equal(from_dev(gs), want[1], "side stream scales")
+
+
+def test_argument_error_writes_nothing():
+    out = torch.full((256,), 0x5A, dtype=torch.uint8, device="cuda")
+    sc = torch.full((4,), 7.0, device="cuda")
+    x = torch.ones(512, device="cuda")
+    with pytest.raises(zq.ZQError):
+        zq.qgz_quantize(x, 48, packed=out, scales=sc)
+    torch.cuda.synchronize()
+    assert bool((out == 0x5A).all()) and bool((sc == 7.0).all())
