@@ -1,0 +1,388 @@
+#!/usr/bin/env python3
+"""Benchmark: one rank's qwZ / qgZ compression step for a GPT-20B layer on one MI355X.
+
+A step is one pass of the whole path over one GPT-20B-shaped layer
+(hidden 6144, FFN 24576: 452,984,832 parameters), inputs resident in HBM:
+
+  qwz_quantize      bf16 weight shard (1/8 = 56,623,104), INT8 blocks of 256,
+                    written into its slot of the gathered buffer
+  qwz_dequantize    the gathered INT8 layer (452,984,832) -> bf16
+  qgz_quantize      fp32 gradient of the layer (452,984,832), INT4 blocks of 128
+  qgz_reduce_level  P = 8 slices of 56,623,104 (one intra-node level)
+  qgz_dequantize    the reduced 56,623,104-element shard -> fp32
+  qgz_reduce_level  3-level chain: P = 2 (m 226,492,416), P = 4 (m 56,623,104),
+                    P = 48 (m 1,179,648)
+  qgz_dequantize    the final 1,179,648-element shard -> fp32
+
+The collectives between the calls (the weight Allgather, the gradient
+all-to-all of each level) are outside this path: their results are placed
+in HBM before timing (peer slices are quantised from seeded fp32 peer
+gradients; a level's local slice is chunk 0 of the previous level's output).
+
+Output: one JSON line.  value = algorithmic bytes of the step / step time.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "achieved HBM GB/s (% of MI355X peak) for qwZ quant/dequant + qgZ reduce, GPT-20B layer"
+HBM_PEAK_GBPS = 8000.0
+WBLOCK, GBLOCK, SHARD = 256, 128, 8
+FANINS = [2, 4, 48]
+
+
+def nsc(n, b):
+    return (n + b - 1) // b
+
+
+def nb4(n):
+    return (n + 1) // 2
+
+
+# algorithmic bytes per call (what the method must read and write)
+def bytes_quant(n, in_b, out_b_per_elem, block):
+    return n * in_b + int(n * out_b_per_elem) + 4 * nsc(n, block)
+
+
+def bytes_qwz_quant(n, in_b, block):
+    return n * in_b + n + 4 * nsc(n, block)
+
+
+def bytes_qwz_deq(n, out_b, block):
+    return n + 4 * nsc(n, block) + n * out_b
+
+
+def bytes_qgz_quant(n, in_b, block):
+    return n * in_b + nb4(n) + 4 * nsc(n, block)
+
+
+def bytes_reduce(P, m, block):
+    return (P + 1) * (nb4(m) + 4 * nsc(m, block))
+
+
+def bytes_qgz_deq(n, out_b, block):
+    return nb4(n) + 4 * nsc(n, block) + n * out_b
+
+
+class Layer20B:
+    """Device buffers and the launch sequence of one step."""
+
+    def __init__(self, n, log):
+        import numpy as np
+        import torch
+
+        import paper_2501_04266_amd as zq
+        from paper_2501_04266_amd import workloads as wl
+
+        self.zq, self.torch, self.np = zq, torch, np
+        self.n = n
+        dev = "cuda"
+        T = torch
+        t0 = time.time()
+        self.host = {}
+        # weights: bf16 N(0, 0.02); the gathered INT8 layer is the Allgather of
+        # all 8 shards' codes, which (shards being block-aligned) equals the
+        # quantisation of the whole layer
+        w = wl.weights(n, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
+        self.host["w"] = w
+        self.w = T.from_numpy(w.view(np.int16)).to(dev).view(T.bfloat16)
+        self.shard = n // SHARD
+        self.codes = T.empty(n, dtype=T.int8, device=dev)
+        self.wscales = T.empty(nsc(n, WBLOCK), dtype=T.float32, device=dev)
+        zq.qwz_quantize(self.w, WBLOCK, codes=self.codes, scales=self.wscales)
+        self.y = T.empty(n, dtype=T.bfloat16, device=dev)
+        log(f"weights ready ({time.time() - t0:.1f}s)")
+
+        # own fp32 gradient N(0, 1e-3) and its INT4 wire format
+        g = wl.normal_f32(n, 1e-3, key=[3, wl.ROLE_OWN_GRAD, 0, 0])
+        self.host["g"] = g
+        self.g = T.from_numpy(g).to(dev)
+        self.gp = T.empty(nb4(n), dtype=T.uint8, device=dev)
+        self.gs = T.empty(nsc(n, GBLOCK), dtype=T.float32, device=dev)
+        zq.qgz_quantize(self.g, GBLOCK, packed=self.gp, scales=self.gs)
+        log(f"gradient ready ({time.time() - t0:.1f}s)")
+
+        # one intra-node level, P = 8 (local rank 0)
+        self.m8 = n // 8
+        self.d8 = self._level_buffers(8, self.m8, self.gp, self.gs, key=(3, 0))
+        self.o8 = (T.empty(nb4(self.m8), dtype=T.uint8, device=dev), T.empty(nsc(self.m8, GBLOCK), device=dev))
+        self.gshard = T.empty(self.m8, dtype=T.float32, device=dev)
+        log(f"P=8 level ready ({time.time() - t0:.1f}s)")
+
+        # 3-level chain 2 / 4 / 48
+        self.chain = []
+        cur_p, cur_s, cur_m = self.gp, self.gs, n
+        for k, P in enumerate(FANINS):
+            m = cur_m // P
+            d = self._level_buffers(P, m, cur_p, cur_s, key=(4, k))
+            o = (T.empty(nb4(m), dtype=T.uint8, device=dev), T.empty(nsc(m, GBLOCK), device=dev))
+            zq.qgz_reduce_level(d[0], d[1], P, m, GBLOCK, packed_out=o[0], scales_out=o[1])
+            self.chain.append((P, m, d, o))
+            cur_p, cur_s, cur_m = o[0], o[1], m
+        self.final = T.empty(cur_m, dtype=T.float32, device=dev)
+        T.cuda.synchronize()
+        log(f"3-level chain ready ({time.time() - t0:.1f}s)")
+
+        # (name, bytes) of each launch, in step order
+        self.calls = [
+            ("qwz_quantize", bytes_qwz_quant(self.shard, 2, WBLOCK)),
+            ("qwz_dequantize", bytes_qwz_deq(n, 2, WBLOCK)),
+            ("qgz_quantize", bytes_qgz_quant(n, 4, GBLOCK)),
+            ("qgz_reduce_level P=8", bytes_reduce(8, self.m8, GBLOCK)),
+            ("qgz_dequantize P=8 shard", bytes_qgz_deq(self.m8, 4, GBLOCK)),
+        ] + [(f"qgz_reduce_level P={P}", bytes_reduce(P, m, GBLOCK)) for P, m, _, _ in self.chain] + [
+            ("qgz_dequantize chain shard", bytes_qgz_deq(cur_m, 4, GBLOCK))]
+
+    def _level_buffers(self, P, m, own_p, own_s, key):
+        """All-to-all receive buffer of one level at local rank 0: slice 0 is
+        chunk 0 of the local input, slices 1..P-1 are INT4 quantisations of
+        seeded fp32 peer chunks."""
+        np, T, zq = self.np, self.torch, self.zq
+        from paper_2501_04266_amd import workloads as wl
+        mb, ms = nb4(m), nsc(m, GBLOCK)
+        pin = T.empty(P * mb, dtype=T.uint8, device="cuda")
+        sin = T.empty(P * ms, dtype=T.float32, device="cuda")
+        pin[:mb].copy_(own_p[:mb])
+        sin[:ms].copy_(own_s[:ms])
+        peers = []
+        for p in range(1, P):
+            xs = wl.normal_f32(m, 1e-3, key=[key[0], wl.ROLE_PEER_GRAD, key[1], p])
+            peers.append(xs)
+            zq.qgz_quantize(T.from_numpy(xs).to("cuda"), GBLOCK, packed=pin[p * mb:(p + 1) * mb],
+                            scales=sin[p * ms:(p + 1) * ms])
+        self.host[("peers",) + tuple(key)] = peers
+        return pin, sin
+
+    def step(self, ev=None):
+        zq = self.zq
+        n, s = self.n, self.shard
+
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+
+        mark(0)
+        zq.qwz_quantize(self.w[:s], WBLOCK, codes=self.codes[:s], scales=self.wscales[:nsc(s, WBLOCK)])
+        mark(1)
+        zq.qwz_dequantize(self.codes, self.wscales, WBLOCK, y=self.y)
+        mark(2)
+        zq.qgz_quantize(self.g, GBLOCK, packed=self.gp, scales=self.gs)
+        mark(3)
+        zq.qgz_reduce_level(self.d8[0], self.d8[1], 8, self.m8, GBLOCK, packed_out=self.o8[0], scales_out=self.o8[1])
+        mark(4)
+        zq.qgz_dequantize(self.o8[0], self.o8[1], self.m8, GBLOCK, y=self.gshard)
+        mark(5)
+        i = 5
+        for P, m, d, o in self.chain:
+            zq.qgz_reduce_level(d[0], d[1], P, m, GBLOCK, packed_out=o[0], scales_out=o[1])
+            i += 1
+            mark(i)
+        P, m, d, o = self.chain[-1]
+        zq.qgz_dequantize(o[0], o[1], m, GBLOCK, y=self.final)
+        mark(i + 1)
+
+
+def oracle_step(L, threads):
+    """The same step on the CPU oracle over the same host inputs; returns
+    (seconds in the timed calls, outputs).  Preparation (gathered codes, peer
+    slices) is untimed, as on the GPU."""
+    import numpy as np
+
+    import oracle
+    oracle.set_threads(threads)
+    n, s = L.n, L.shard
+    w, g = L.host["w"], L.host["g"]
+    codes_all, sc_all = oracle.qwz_quantize(w, WBLOCK, "bf16")       # the gathered layer (prep)
+    outs, t = {}, 0.0
+
+    def timed(fn, *a):
+        nonlocal t
+        t0 = time.perf_counter()
+        r = fn(*a)
+        t += time.perf_counter() - t0
+        return r
+
+    outs["shard_codes"] = timed(oracle.qwz_quantize, w[:s], WBLOCK, "bf16")
+    outs["y"] = timed(oracle.qwz_dequantize, codes_all, sc_all, WBLOCK, "bf16")
+    gp, gs = timed(oracle.qgz_quantize, g, GBLOCK, "f32")
+
+    def level(P, m, own_p, own_s, key):
+        mb, ms = nb4(m), nsc(m, GBLOCK)
+        ps, ss = [own_p[:mb]], [own_s[:ms]]
+        for xs in L.host[("peers",) + key]:
+            a, b = oracle.qgz_quantize(xs, GBLOCK, "f32")
+            ps.append(a)
+            ss.append(b)
+        return np.concatenate(ps), np.concatenate(ss)
+
+    pin, sin = level(8, L.m8, gp, gs, (3, 0))
+    o8 = timed(oracle.qgz_reduce_level, pin, sin, 8, L.m8, GBLOCK)
+    outs["gshard"] = timed(oracle.qgz_dequantize, o8[0], o8[1], L.m8, GBLOCK, "f32")
+    cur_p, cur_s, cur_m = gp, gs, n
+    for k, P in enumerate(FANINS):
+        m = cur_m // P
+        pin, sin = level(P, m, cur_p, cur_s, (4, k))
+        cur_p, cur_s = timed(oracle.qgz_reduce_level, pin, sin, P, m, GBLOCK)
+        outs[f"chain{k}"] = (cur_p, cur_s)
+        cur_m = m
+    outs["final"] = timed(oracle.qgz_dequantize, cur_p, cur_s, cur_m, GBLOCK, "f32")
+    outs["gp"] = (gp, gs)
+    return t, outs
+
+
+def check_against_oracle(L, outs):
+    """Bit-exact comparison of every step output with the oracle's."""
+    import numpy as np
+    T = L.torch
+
+    def host(t):
+        if t.dtype == T.bfloat16:
+            return t.view(T.int16).cpu().numpy().view(np.uint16)
+        return t.cpu().numpy()
+
+    pairs = [
+        ("shard codes", host(L.codes[:L.shard]), outs["shard_codes"][0]),
+        ("shard scales", host(L.wscales[:nsc(L.shard, WBLOCK)]), outs["shard_codes"][1]),
+        ("dequant bf16", host(L.y), outs["y"]),
+        ("grad packed", host(L.gp), outs["gp"][0]),
+        ("grad scales", host(L.gs), outs["gp"][1]),
+        ("P=8 shard fp32", host(L.gshard), outs["gshard"]),
+        ("final fp32", host(L.final), outs["final"]),
+    ]
+    for k, (P, m, d, o) in enumerate(L.chain):
+        pairs.append((f"chain level {k} packed", host(o[0]), outs[f"chain{k}"][0]))
+        pairs.append((f"chain level {k} scales", host(o[1]), outs[f"chain{k}"][1]))
+    bad = [name for name, a, b in pairs if a.tobytes() != np.ascontiguousarray(b).tobytes()]
+    return bad
+
+
+def load_traffic(kernel_name):
+    """HBM bytes per launch from committed rocprofv3 PMC summaries, if they
+    were taken on the current kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+    if not os.path.exists(path):
+        return None
+    d = json.load(open(path))
+    src = os.path.join(ROOT, "paper_2501_04266_amd", "csrc", "zq_kernels.hip")
+    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if d.get("kernel_source_sha256_16") != h:
+        return None
+    ent = d.get("kernels", {}).get(kernel_name)
+    return ent.get("bytes_per_launch") if ent else None
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
+    ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
+    ap.add_argument("--n", type=int, default=0, help=argparse.SUPPRESS)  # smaller layer for quick checks
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this path runs on one GPU only (the P slices of each level are held in one "
+              "GPU's HBM); --gpus must be 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2501_04266_amd as zq
+    from paper_2501_04266_amd import workloads as wl
+
+    if not os.path.exists(zq.LIB_PATH):
+        from paper_2501_04266_amd import build as zbuild
+        zbuild.build()
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+
+    def log(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    n = args.n or wl.N_20B
+    L = Layer20B(n, log)
+    ncalls = len(L.calls)
+    for _ in range(args.warmup):
+        L.step()
+    torch.cuda.synchronize()
+    log(f"warmup {args.warmup} done")
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ncalls + 1)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        L.step(evs[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+
+    per_call_ms = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(ncalls)]
+                            for k in range(args.steps)]).mean(axis=0)
+    step_bytes = sum(b for _, b in L.calls)
+    value = step_bytes / (ms_per_step * 1e-3) / 1e9
+    kernels = []
+    for (name, b), ms in zip(L.calls, per_call_ms):
+        kernels.append({"call": name, "bytes": b, "us": round(ms * 1e3, 2),
+                        "GBps": round(b / (ms * 1e-3) / 1e9, 1)})
+    dom = max(range(ncalls), key=lambda i: per_call_ms[i])
+    dom_name, dom_bytes = L.calls[dom]
+    achieved = dom_bytes / (per_call_ms[dom] * 1e-3) / 1e9
+    traffic = load_traffic(dom_name)
+
+    # practical ceiling: a plain device-to-device copy of 1 GiB
+    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    copy_gbps = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
+
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "gpt-20b-layer qwZ/qgZ step (h=6144, ffn=24576, n=452,984,832): "
+                               "qwz shard 1/8 bf16 B=256 + gathered dequant -> bf16; qgz fp32 B=128, "
+                               "P=8 level + 3-level chain P=2/4/48, final dequant -> fp32",
+                   "n": n, "step_bytes": step_bytes, "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 1),
+                   "elements_per_s": round(sum(nn for nn in (L.shard, n, n, L.m8 * 8, L.m8)) / (ms_per_step * 1e-3))},
+        "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "bytes_per_launch": dom_bytes, "us_per_launch": round(per_call_ms[dom] * 1e3, 2)},
+        "kernels": kernels,
+        "copy_ceiling_GBps": round(copy_gbps, 1),
+    }
+
+    if not args.no_cpu_baseline:
+        threads = args.cpu_threads or max(1, len(os.sched_getaffinity(0)))
+        log(f"oracle step on {threads} threads ...")
+        secs, outs = oracle_step(L, threads)
+        bad = check_against_oracle(L, outs)
+        out["cpu_baseline"] = {"value": round(step_bytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
+                               "kind": "oracle", "seconds": round(secs, 2),
+                               "sample": "one full step of the same workload (all calls, full sizes)"}
+        out["parity"] = "bit-exact vs oracle (all step outputs)" if not bad else f"MISMATCH: {bad}"
+        log(f"oracle {secs:.1f}s; parity: {out['parity']}")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -142,8 +142,13 @@ struct Elem<ZQ_BF16> {
 __device__ __forceinline__ float h2f(uint32_t bits16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
 }
+// binary32 -> binary16, nearest even (v_cvt_f16_f32).  The empty asm pins v
+// as a materialised binary32 value: without it the compiler folds a preceding
+// fp32 multiply and this narrowing into one v_fma_mixlo_f16, which rounds the
+// exact product once instead of rounding it to binary32 first.
 __device__ __forceinline__ uint32_t f2h(float v) {
-  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);  // v_cvt_f16_f32, nearest even
+  asm("" : "+v"(v));
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
 }
 
 template <>

@@ -121,6 +121,49 @@ def test_dequantize_golden_rounding():
     assert_bits_equal(from_dev(y), oracle.qgz_dequantize(packed, s, 32, 32, "f16"), "f16 subnormal ties")
 
 
+def _f16_tie_cases(qmax, count, seed):
+    """(code, scale) pairs whose binary32 product is an exact binary16 tie
+    (13 dropped bits = 1000000000000b) in the normal range and is itself a
+    rounded value, so rounding the exact product once to binary16 can give a
+    different answer than the definition (round to binary32, then to
+    binary16).  Found by search on the CPU."""
+    g = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        q = g.integers(1, qmax + 1, 1 << 20) * g.choice([-1, 1], 1 << 20)
+        s = (2.0 ** g.uniform(-10, -4, 1 << 20)).astype(np.float32)
+        prod = (q.astype(np.float32) * s).astype(np.float32)
+        u = prod.view(np.uint32)
+        exact = q.astype(np.float64) * s.astype(np.float64)
+        hit = ((u & 0x1FFF) == 0x1000) & (np.abs(prod) >= 2.0 ** -14) & (exact != prod.astype(np.float64))
+        for i in np.flatnonzero(hit):
+            out.append((int(q[i]), float(s[i])))
+    return out[:count]
+
+
+@pytest.mark.parametrize("op", ["qwz", "qgz"])
+def test_dequantize_f16_ties_of_fp32_products(op):
+    """Regression: fp16 output must round the binary32 product, not the exact
+    one (a fused multiply-narrow instruction gets these wrong)."""
+    block, nblk = 32, 256
+    cases = _f16_tie_cases(127 if op == "qwz" else 7, nblk, 77)
+    g = np.random.default_rng(3)
+    codes = g.integers(-7, 8, nblk * block).astype(np.int64)
+    scales = np.array([s for _, s in cases], np.float32)
+    codes[::block] = [q for q, _ in cases]
+    if op == "qwz":
+        c = codes.astype(np.int8)
+        want = oracle.qwz_dequantize(c, scales, block, "f16")
+        y = zq.qwz_dequantize(to_dev(c), to_dev(scales), block, out_dtype=torch.float16)
+    else:
+        nib = codes & 0xF
+        c = (nib[0::2] | (nib[1::2] << 4)).astype(np.uint8)
+        want = oracle.qgz_dequantize(c, scales, codes.size, block, "f16")
+        y = zq.qgz_dequantize(to_dev(c), to_dev(scales), codes.size, block, out_dtype=torch.float16)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(y), want, f"{op} f16 ties")
+
+
 def _slices(P, m, block, seed, scale_spread=True):
     g = np.random.default_rng(seed)
     xs = []
