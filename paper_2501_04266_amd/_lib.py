@@ -11,7 +11,7 @@ import os
 import torch  # noqa: F401  -- loads torch's HIP runtime first, so libzq binds to the same one
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libzq.so")
+LIB_PATH = os.environ.get("ZQ_LIBRARY") or os.path.join(_PKG, "libzq.so")
 
 ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
 STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",

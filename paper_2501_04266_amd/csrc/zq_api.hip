@@ -2,12 +2,11 @@
 // the host, grid sizing, and launches on the caller's stream.
 //
 // Every check runs before anything is enqueued, so an argument error writes
-// no output byte.  The library allocates nothing and keeps no per-call state;
-// the only process-wide value is the optional workgroup cap read once from
-// ZQ_MAX_WORKGROUPS (used to vary launch geometry in determinism tests).
+// no output byte.  The library allocates nothing and keeps no state.  Each
+// launch covers its whole tensor (one tile per wave), so the grid size follows
+// from n alone.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
-#include <stdlib.h>
 
 #include <tuple>
 #include <utility>
@@ -19,20 +18,14 @@ namespace {
 
 using namespace zq;
 
-int max_workgroups() {
-  static const int cap = [] {
-    const char* e = getenv("ZQ_MAX_WORKGROUPS");
-    long v = e ? strtol(e, nullptr, 10) : 0;
-    return (v >= 1 && v <= (1L << 30)) ? (int)v : 8192;
-  }();
-  return cap;
-}
+constexpr int64_t kMaxGrid = 0x7fffffff;  // workgroups per launch
 
-unsigned grid_for(int64_t units, int64_t units_per_wg) {
-  int64_t g = (units + units_per_wg - 1) / units_per_wg;
+// Workgroups to cover `units` at `units_per_wg` each (0 if it exceeds the
+// launch limit; callers turn that into ZQ_E_SIZE before anything is enqueued).
+int64_t grid_for(int64_t units, int64_t units_per_wg, bool remap = false) {
+  int64_t g = launch_grid((units + units_per_wg - 1) / units_per_wg, remap);
   if (g < 1) g = 1;
-  if (g > max_workgroups()) g = max_workgroups();
-  return (unsigned)g;
+  return g > kMaxGrid ? 0 : g;
 }
 
 // Launch with the kernel's exact parameter types; returns ZQ_E_HIP when the
@@ -96,13 +89,15 @@ int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, floa
   const int64_t out_bytes = qbits == 8 ? n : (n + 1) / 2;
   if (any_overlap({{out, out_bytes}, {scales, 4 * nb}}, {{x, n * elem_bytes(xt)}})) return ZQ_E_ALIAS;
 
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const int64_t nfull = n / block;
+  const int64_t blocks_per_wave = 64 / (block / quant_elems((int)elem_bytes(xt), block));
+  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64);
+  if (grid == 0) return ZQ_E_SIZE;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
   int rc = ZQ_OK;
   if (nfull > 0) {
-    const int64_t blocks_per_wave = 1024 / block;  // 64 lanes x 16 elements
-    const int64_t waves = (nfull + blocks_per_wave - 1) / blocks_per_wave;
-    rc = launch(quant_kernel(xt, qbits, lgB), grid_for(waves, kThreads / 64), kThreads, st, x, nfull, out, scales);
+    rc = launch(quant_kernel(xt, qbits, lgB), (unsigned)grid, kQuantThreads, st, x, nfull, out, scales);
     if (rc != ZQ_OK) return rc;
   }
   const int64_t rest = n - nfull * block;
@@ -126,11 +121,17 @@ int dequantize(const void* codes, const float* scales, int64_t n, int32_t block,
   const int64_t in_bytes = qbits == 8 ? n : (n + 1) / 2;
   if (any_overlap({{y, n * elem_bytes(yt)}}, {{codes, in_bytes}, {scales, 4 * nb}})) return ZQ_E_ALIAS;
 
+  // thread g < n/E dequantises elements [gE, gE + E); the n % E leftovers go
+  // to the following threads, one element each
+  const int64_t E = qbits == 8 ? deq8_elems((int)elem_bytes(yt)) : deq4_elems((int)elem_bytes(yt));
+  const int64_t grid = grid_for(n / E + n % E, kThreads, qbits == 8 && ZQ_REMAP_DEQ8);
+  if (grid == 0) return ZQ_E_SIZE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  const unsigned grid = grid_for(n >> 4, kThreads);
   if (qbits == 8)
-    return launch(dequant8_kernel(yt), grid, kThreads, st, static_cast<const int8_t*>(codes), scales, n, lgB, y);
-  return launch(dequant4_kernel(yt), grid, kThreads, st, static_cast<const uint8_t*>(codes), scales, n, lgB, y);
+    return launch(dequant8_kernel(yt), (unsigned)grid, kThreads, st, static_cast<const int8_t*>(codes), scales, n,
+                  lgB, y);
+  return launch(dequant4_kernel(yt), (unsigned)grid, kThreads, st, static_cast<const uint8_t*>(codes), scales, n,
+                lgB, y);
 }
 
 }  // namespace
@@ -172,19 +173,21 @@ int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P
                   {{packed_in, slice_bytes * P}, {scales_in, 4 * nb * P}}))
     return ZQ_E_ALIAS;
 
+  // every slice starts 16-byte aligned when m % 32 == 0: vector path over the
+  // full blocks, 64 lanes x 32 elements per wave
+  const bool vector_path = m % 32 == 0;
+  const int64_t nfull = vector_path ? m / block : 0;
+  const int64_t blocks_per_wave = 64 / (block / kReduceElems);
+  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64);
+  if (grid == 0) return ZQ_E_SIZE;
+
   hipStream_t st = static_cast<hipStream_t>(stream);
-  int64_t generic_from = 0;
-  if (m % 32 == 0) {
-    // every slice starts 16-byte aligned: vector path over the full blocks
-    const int64_t nfull = m / block;
-    if (nfull > 0) {
-      const int64_t waves = (nfull * block + 2047) / 2048;  // 64 lanes x 32 elements
-      int rc = launch(reduce_kernel(lgB), grid_for(waves, kThreads / 64), kThreads, st, packed_in, scales_in, (int)P,
-                      slice_bytes, nb, nfull, packed_out, scales_out);
-      if (rc != ZQ_OK) return rc;
-    }
-    generic_from = nfull;
+  if (nfull > 0) {
+    int rc = launch(reduce_kernel(lgB), (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb,
+                    nfull, packed_out, scales_out);
+    if (rc != ZQ_OK) return rc;
   }
+  const int64_t generic_from = nfull;
   // remaining blocks (a short last block, or all of them when slices are not
   // 16-byte aligned): one wave per block
   for (int64_t b0 = generic_from; b0 < nb; b0 += (1LL << 30)) {

@@ -7,15 +7,17 @@
 // written out in include/zq.h.
 //
 // All kernels are streaming, HBM-bound work (no contraction, so no MFMA):
-//   * wave64 tiles with 16-byte loads/stores per lane, consecutive lanes on
-//     consecutive addresses;
+//   * one tile of 64 lanes x E elements per wave, launches covering the whole
+//     tensor, nontemporal loads and stores (data is touched once);
 //   * per-block absmax reduced across the lanes of a block with DPP row
 //     permutes (quad_perm, row_half_mirror, row_mirror) -- no LDS round trip;
 //   * rounding to nearest-even by adding 1.5*2^23, which leaves the code as
 //     two's complement in the low mantissa bits, then byte/nibble packing
 //     with v_perm_b32;
-//   * grid-stride loops over wave tiles; every wave of a launch runs the same
-//     number of iterations, so cross-lane ops always see full waves.
+//   * the reduce level, the one kernel with real arithmetic per byte (P
+//     multiplies and adds per output element), converts a nibble with one
+//     v_cvt_off_f32_i4 (q/16 exactly) and multiplies by 16*s, which is exact,
+//     so every product is still fl(q*s).
 //
 // Floating point: built with -ffp-contract=off (and the pragma below) so a*b+c
 // is never fused; fp32 division is the correctly rounded sequence; fp32 and
@@ -28,11 +30,51 @@
 
 #pragma clang fp contract(off)
 
+// Nontemporal hints per kernel family: bit 0 = loads, bit 1 = stores.  Data
+// streamed once gains from them; a kernel whose input was just written by the
+// previous call (the dequantiser after a reduce level) loses its cache hits.
+#ifndef ZQ_NT_QUANT
+#define ZQ_NT_QUANT 3
+#endif
+#ifndef ZQ_NT_DEQ8
+#define ZQ_NT_DEQ8 3
+#endif
+#ifndef ZQ_NT_DEQ4
+#define ZQ_NT_DEQ4 0
+#endif
+#ifndef ZQ_NT_REDUCE
+#define ZQ_NT_REDUCE 3
+#endif
+// Scale arrays are written 4 bytes per block, i.e. in partial cache lines:
+// plain stores let L2 merge them into full lines before write-back.
+#ifndef ZQ_NT_SCALES
+#define ZQ_NT_SCALES 0
+#endif
+// slices loaded ahead per batch in the reduce level
+#ifndef ZQ_REDUCE_U
+#define ZQ_REDUCE_U 4
+#endif
+
 namespace zq {
 namespace {
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
 constexpr float kRoundMagic = 12582912.0f;  // 1.5 * 2^23
 constexpr float kFlushBelow = 0x1p-119f;    // absmax below this: zero block
+constexpr float kMaxFloat = 3.40282346638528859812e+38f;
+
+template <int NT, typename T>
+__device__ __forceinline__ T ld(const T* p) {
+  if constexpr (NT & 1) return __builtin_nontemporal_load(p);
+  else return *p;
+}
+template <int NT, typename T>
+__device__ __forceinline__ void st(T* p, T v) {
+  if constexpr (NT & 2) __builtin_nontemporal_store(v, p);
+  else *p = v;
+}
 
 __device__ __forceinline__ uint32_t f2u(float f) { return __builtin_bit_cast(uint32_t, f); }
 __device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(float, u); }
@@ -48,6 +90,31 @@ __device__ __forceinline__ uint32_t code_bits(float v, float r) {
 // INT4 code (two's complement nibble k of w) as float.
 __device__ __forceinline__ float nib_to_f32(uint32_t w, int k) {
   return (float)((int32_t)(w << (28 - 4 * k)) >> 28);
+}
+
+// q/16 for the two's-complement low nibble of byte BYTE of w, in one
+// instruction (v_cvt_off_f32_i4 with an SDWA byte select).
+template <int BYTE>
+__device__ __forceinline__ float nib_over_16(uint32_t w) {
+  float f;
+  if constexpr (BYTE == 0)
+    asm("v_cvt_off_f32_i4_sdwa %0, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_0" : "=v"(f) : "v"(w));
+  else if constexpr (BYTE == 1)
+    asm("v_cvt_off_f32_i4_sdwa %0, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_1" : "=v"(f) : "v"(w));
+  else if constexpr (BYTE == 2)
+    asm("v_cvt_off_f32_i4_sdwa %0, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_2" : "=v"(f) : "v"(w));
+  else
+    asm("v_cvt_off_f32_i4_sdwa %0, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:BYTE_3" : "=v"(f) : "v"(w));
+  return f;
+}
+
+// The 8 nibbles of w, each as q/16 (element order: low nibble of byte 0 first).
+__device__ __forceinline__ void nibbles_over_16(uint32_t w, float* o) {
+  const uint32_t h = w >> 4;
+  o[0] = nib_over_16<0>(w); o[1] = nib_over_16<0>(h);
+  o[2] = nib_over_16<1>(w); o[3] = nib_over_16<1>(h);
+  o[4] = nib_over_16<2>(w); o[5] = nib_over_16<2>(h);
+  o[6] = nib_over_16<3>(w); o[7] = nib_over_16<3>(h);
 }
 
 // Max over the L lanes of an aligned lane group (L a power of two <= 64).
@@ -80,64 +147,49 @@ __device__ __forceinline__ uint32_t pack_nibbles8(const uint32_t* m) {
   return (ev & 0x0f0f0f0fu) | ((od << 4) & 0xf0f0f0f0u);
 }
 
-// ------------------------------------------------------------------ element I/O
+// ------------------------------------------------------------------ raw I/O
 
-template <int DT>
-struct Elem;
-
-template <>
-struct Elem<ZQ_F32> {
-  __device__ static void load16(const void* p, int64_t i, float (&v)[16]) {
-    const float4* q = reinterpret_cast<const float4*>(static_cast<const float*>(p) + i);
+template <int NT, int NW>
+__device__ __forceinline__ void load_words(const void* p, uint32_t (&w)[NW]) {
+  if constexpr (NW % 4 == 0) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      float4 f = q[k];
-      v[4 * k] = f.x; v[4 * k + 1] = f.y; v[4 * k + 2] = f.z; v[4 * k + 3] = f.w;
+    for (int k = 0; k < NW / 4; ++k) {
+      const u32x4 t = ld<NT>(static_cast<const u32x4*>(p) + k);
+      w[4 * k] = t.x; w[4 * k + 1] = t.y; w[4 * k + 2] = t.z; w[4 * k + 3] = t.w;
     }
+  } else if constexpr (NW == 2) {
+    const u32x2 t = ld<NT>(static_cast<const u32x2*>(p));
+    w[0] = t.x; w[1] = t.y;
+  } else {
+    static_assert(NW == 1, "words");
+    w[0] = ld<NT>(static_cast<const uint32_t*>(p));
   }
-  __device__ static float load1(const void* p, int64_t i) { return static_cast<const float*>(p)[i]; }
-  __device__ static void store16(void* p, int64_t i, const float (&v)[16]) {
-    float4* q = reinterpret_cast<float4*>(static_cast<float*>(p) + i);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) q[k] = make_float4(v[4 * k], v[4 * k + 1], v[4 * k + 2], v[4 * k + 3]);
-  }
-  __device__ static void store1(void* p, int64_t i, float v) { static_cast<float*>(p)[i] = v; }
-};
+}
 
-// bf16 <-> f32: widening is a 16-bit shift; narrowing is v_cvt_pk_bf16_f32
-// (round to nearest even).
+template <int NT, int NW>
+__device__ __forceinline__ void store_words(void* p, const uint32_t (&w)[NW]) {
+  if constexpr (NW % 4 == 0) {
+#pragma unroll
+    for (int k = 0; k < NW / 4; ++k)
+      st<NT>(static_cast<u32x4*>(p) + k, u32x4{w[4 * k], w[4 * k + 1], w[4 * k + 2], w[4 * k + 3]});
+  } else if constexpr (NW == 2) {
+    st<NT>(static_cast<u32x2*>(p), u32x2{w[0], w[1]});
+  } else {
+    static_assert(NW == 1, "words");
+    st<NT>(static_cast<uint32_t*>(p), w[0]);
+  }
+}
+
+// ------------------------------------------------------------------ element formats
+
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 
+// two binary32 -> two bfloat16 (v_cvt_pk_bf16_f32, nearest even)
 __device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
   f32x2_t v = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
-
-template <>
-struct Elem<ZQ_BF16> {
-  __device__ static void load16(const void* p, int64_t i, float (&v)[16]) {
-    const uint4* q = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
-    uint4 a = q[0], b = q[1];
-    uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      v[2 * k] = u2f(w[k] << 16);
-      v[2 * k + 1] = u2f(w[k] & 0xffff0000u);
-    }
-  }
-  __device__ static float load1(const void* p, int64_t i) {
-    return u2f((uint32_t)static_cast<const uint16_t*>(p)[i] << 16);
-  }
-  __device__ static void store16(void* p, int64_t i, const float (&v)[16]) {
-    uint4* q = reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + i);
-    q[0] = make_uint4(bf16x2_bits(v[0], v[1]), bf16x2_bits(v[2], v[3]), bf16x2_bits(v[4], v[5]), bf16x2_bits(v[6], v[7]));
-    q[1] = make_uint4(bf16x2_bits(v[8], v[9]), bf16x2_bits(v[10], v[11]), bf16x2_bits(v[12], v[13]), bf16x2_bits(v[14], v[15]));
-  }
-  __device__ static void store1(void* p, int64_t i, float v) {
-    static_cast<uint16_t*>(p)[i] = (uint16_t)(bf16x2_bits(v, 0.0f) & 0xffffu);
-  }
-};
 
 __device__ __forceinline__ float h2f(uint32_t bits16) {
   return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
@@ -151,82 +203,122 @@ __device__ __forceinline__ uint32_t f2h(float v) {
   return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
 }
 
-template <>
-struct Elem<ZQ_F16> {
-  __device__ static void load16(const void* p, int64_t i, float (&v)[16]) {
-    const uint4* q = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + i);
-    uint4 a = q[0], b = q[1];
-    uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+template <int DT>
+constexpr int elem_size() { return DT == ZQ_F32 ? 4 : 2; }
+
+// E consecutive elements from element index i, widened to binary32 (exact).
+template <int NT, int DT, int E>
+__device__ __forceinline__ void load_elems(const void* p, int64_t i, float (&v)[E]) {
+  constexpr int NW = E * elem_size<DT>() / 4;
+  uint32_t w[NW];
+  load_words<NT, NW>(static_cast<const char*>(p) + i * elem_size<DT>(), w);
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
+  for (int k = 0; k < NW; ++k) {
+    if constexpr (DT == ZQ_F32) {
+      v[k] = u2f(w[k]);
+    } else if constexpr (DT == ZQ_BF16) {
+      v[2 * k] = u2f(w[k] << 16);
+      v[2 * k + 1] = u2f(w[k] & 0xffff0000u);
+    } else {
       v[2 * k] = h2f(w[k] & 0xffffu);
       v[2 * k + 1] = h2f(w[k] >> 16);
     }
   }
-  __device__ static float load1(const void* p, int64_t i) { return h2f(static_cast<const uint16_t*>(p)[i]); }
-  __device__ static void store16(void* p, int64_t i, const float (&v)[16]) {
-    uint4* q = reinterpret_cast<uint4*>(static_cast<uint16_t*>(p) + i);
-    uint32_t w[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) w[k] = f2h(v[2 * k]) | (f2h(v[2 * k + 1]) << 16);
-    q[0] = make_uint4(w[0], w[1], w[2], w[3]);
-    q[1] = make_uint4(w[4], w[5], w[6], w[7]);
-  }
-  __device__ static void store1(void* p, int64_t i, float v) { static_cast<uint16_t*>(p)[i] = (uint16_t)f2h(v); }
-};
-
-__device__ __forceinline__ int64_t wave_id() {
-  return (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
 }
-__device__ __forceinline__ int64_t wave_count() { return (int64_t)gridDim.x * (blockDim.x >> 6); }
+
+// E binary32 values narrowed (nearest even) and stored from element index i.
+template <int NT, int DT, int E>
+__device__ __forceinline__ void store_elems(void* p, int64_t i, const float (&v)[E]) {
+  constexpr int NW = E * elem_size<DT>() / 4;
+  uint32_t w[NW];
+#pragma unroll
+  for (int k = 0; k < NW; ++k) {
+    if constexpr (DT == ZQ_F32) w[k] = f2u(v[k]);
+    else if constexpr (DT == ZQ_BF16) w[k] = bf16x2_bits(v[2 * k], v[2 * k + 1]);
+    else w[k] = f2h(v[2 * k]) | (f2h(v[2 * k + 1]) << 16);
+  }
+  store_words<NT, NW>(static_cast<char*>(p) + i * elem_size<DT>(), w);
+}
+
+template <int DT>
+__device__ __forceinline__ float load1(const void* p, int64_t i) {
+  if constexpr (DT == ZQ_F32) return static_cast<const float*>(p)[i];
+  else if constexpr (DT == ZQ_BF16) return u2f((uint32_t)static_cast<const uint16_t*>(p)[i] << 16);
+  else return h2f(static_cast<const uint16_t*>(p)[i]);
+}
+
+template <int DT>
+__device__ __forceinline__ void store1(void* p, int64_t i, float v) {
+  if constexpr (DT == ZQ_F32) static_cast<float*>(p)[i] = v;
+  else if constexpr (DT == ZQ_BF16) static_cast<uint16_t*>(p)[i] = (uint16_t)(bf16x2_bits(v, 0.0f) & 0xffffu);
+  else static_cast<uint16_t*>(p)[i] = (uint16_t)f2h(v);
+}
+
+// Logical workgroup index under the XCD remap (see zq_internal.h).  Indices
+// at or beyond `tiles` belong to padding workgroups, which do nothing.
+template <bool REMAP>
+__device__ __forceinline__ int64_t group_index() {
+  if constexpr (REMAP) {
+    const int64_t per = gridDim.x / kXcds;
+    return (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+  } else {
+    return blockIdx.x;
+  }
+}
+
+__device__ __forceinline__ int64_t wave_id() { return (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); }
 
 }  // namespace
 
 // ------------------------------------------------------------------ quantise
-// Full blocks only.  A lane owns 16 consecutive elements; L = B/16 lanes hold
-// one block; a wave tile is 64/L blocks.
+// Full blocks only.  A lane owns E consecutive elements; L = B/E lanes hold
+// one block; one wave tile is 64/L blocks.
 
 template <int DT, int QBITS, int B>
-__global__ void __launch_bounds__(kThreads) k_quantize(const void* __restrict__ x, int64_t nfull,
+__global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restrict__ x, int64_t nfull,
                                                        uint8_t* __restrict__ out, float* __restrict__ scales) {
-  constexpr int E = 16, L = B / E, BPW = 64 / L;
+  constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
+  static_assert(E % 4 == 0 && L >= 1 && L <= 64, "lane layout");
   const int lane = threadIdx.x & 63;
-  const int64_t ntiles = (nfull + BPW - 1) / BPW;
-  for (int64_t t = wave_id(); t < ntiles; t += wave_count()) {
-    const int64_t blk = t * BPW + lane / L;
-    const bool valid = blk < nfull;
-    const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
-    float v[E];
-    if (valid) {
-      Elem<DT>::load16(x, e0, v);
+  const int64_t blk = wave_id() * BPW + lane / L;
+  const bool valid = blk < nfull;
+  const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
+  float v[E];
+  if (valid) {
+    load_elems<ZQ_NT_QUANT, DT, E>(x, e0, v);
+  } else {
+#pragma unroll
+    for (int k = 0; k < E; ++k) v[k] = 0.0f;
+  }
+  float a = fabsf(v[0]);
+#pragma unroll
+  for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(v[k]));
+  const float amax = u2f(group_max<L>(f2u(a)));
+  float s = 0.0f, r = 0.0f;
+  if (amax >= kFlushBelow) {
+    s = amax / QMAX;
+    r = QMAX / amax;
+  }
+  uint32_t m[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) m[k] = code_bits(v[k], r);
+  if (valid) {
+    if constexpr (QBITS == 8) {
+      uint32_t w[E / 4];
+#pragma unroll
+      for (int k = 0; k < E / 4; ++k) w[k] = pack_bytes4(m[4 * k], m[4 * k + 1], m[4 * k + 2], m[4 * k + 3]);
+      store_words<ZQ_NT_QUANT, E / 4>(out + e0, w);
+    } else if constexpr (E == 4) {
+      const uint32_t h = (m[0] & 0xfu) | ((m[1] & 0xfu) << 4) | ((m[2] & 0xfu) << 8) | ((m[3] & 0xfu) << 12);
+      st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(out + (e0 >> 1)), (uint16_t)h);
     } else {
+      uint32_t w[E / 8];
 #pragma unroll
-      for (int k = 0; k < E; ++k) v[k] = 0.0f;
+      for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
+      store_words<ZQ_NT_QUANT, E / 8>(out + (e0 >> 1), w);
     }
-    float a = fabsf(v[0]);
-#pragma unroll
-    for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(v[k]));
-    const float amax = u2f(group_max<L>(f2u(a)));
-    float s = 0.0f, r = 0.0f;
-    if (amax >= kFlushBelow) {
-      s = amax / QMAX;
-      r = QMAX / amax;
-    }
-    uint32_t m[E];
-#pragma unroll
-    for (int k = 0; k < E; ++k) m[k] = code_bits(v[k], r);
-    if (valid) {
-      if constexpr (QBITS == 8) {
-        uint4 o = make_uint4(pack_bytes4(m[0], m[1], m[2], m[3]), pack_bytes4(m[4], m[5], m[6], m[7]),
-                             pack_bytes4(m[8], m[9], m[10], m[11]), pack_bytes4(m[12], m[13], m[14], m[15]));
-        *reinterpret_cast<uint4*>(out + e0) = o;
-      } else {
-        uint2 o = make_uint2(pack_nibbles8(m), pack_nibbles8(m + 8));
-        *reinterpret_cast<uint2*>(out + (e0 >> 1)) = o;
-      }
-      if (lane % L == 0) scales[blk] = s;
-    }
+    if (lane % L == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
   }
 }
 
@@ -237,7 +329,7 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
   const int lane = threadIdx.x;
   float a = 0.0f;
-  for (int j = lane; j < len; j += 64) a = fmaxf(a, fabsf(Elem<DT>::load1(x, start + j)));
+  for (int j = lane; j < len; j += 64) a = fmaxf(a, fabsf(load1<DT>(x, start + j)));
   const float amax = u2f(wave_max(f2u(a)));
   float s = 0.0f, r = 0.0f;
   if (amax >= kFlushBelow) {
@@ -245,11 +337,11 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
     r = QMAX / amax;
   }
   if constexpr (QBITS == 8) {
-    for (int j = lane; j < len; j += 64) out[start + j] = (uint8_t)code_bits(Elem<DT>::load1(x, start + j), r);
+    for (int j = lane; j < len; j += 64) out[start + j] = (uint8_t)code_bits(load1<DT>(x, start + j), r);
   } else {
     for (int k = lane; 2 * k < len; k += 64) {
-      uint32_t lo = code_bits(Elem<DT>::load1(x, start + 2 * k), r);
-      uint32_t hi = (2 * k + 1 < len) ? code_bits(Elem<DT>::load1(x, start + 2 * k + 1), r) : 0u;
+      uint32_t lo = code_bits(load1<DT>(x, start + 2 * k), r);
+      uint32_t hi = (2 * k + 1 < len) ? code_bits(load1<DT>(x, start + 2 * k + 1), r) : 0u;
       out[(start >> 1) + k] = (uint8_t)((lo & 0xfu) | ((hi & 0xfu) << 4));
     }
   }
@@ -257,130 +349,152 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
 }
 
 // ------------------------------------------------------------------ INT8 dequantise
-// A thread owns 16 consecutive codes (one 16-byte load), all in one block.
+// Thread g < n/E owns codes [gE, gE + E) (one block); the n % E leftover
+// elements go to the next threads, one each.
 
 template <int DT>
 __global__ void __launch_bounds__(kThreads) k_qwz_dequant(const int8_t* __restrict__ codes,
                                                           const float* __restrict__ scales, int64_t n, int lgB,
                                                           void* __restrict__ y) {
-  const int64_t ngroups = n >> 4;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t g = tid; g < ngroups; g += nthreads) {
-    const int64_t e0 = g << 4;
-    const uint4 w4 = *reinterpret_cast<const uint4*>(codes + e0);
-    const float s = scales[e0 >> lgB];
-    const uint32_t w[4] = {w4.x, w4.y, w4.z, w4.w};
-    float v[16];
+  constexpr int E = deq8_elems(elem_size<DT>());
+  const int64_t ngroups = n / E;
+  const int64_t gid = group_index<ZQ_REMAP_DEQ8 != 0>() * blockDim.x + threadIdx.x;
+  if (gid < ngroups) {
+    const int64_t e0 = gid * E;
+    uint32_t w[E / 4];
+    load_words<ZQ_NT_DEQ8, E / 4>(codes + e0, w);
+    const float s = ld<ZQ_NT_DEQ8>(scales + (e0 >> lgB));
+    float v[E];
 #pragma unroll
-    for (int k = 0; k < 16; ++k) v[k] = (float)(int32_t)(int8_t)(w[k >> 2] >> (8 * (k & 3))) * s;
-    Elem<DT>::store16(y, e0, v);
-  }
-  const int64_t rest = n - (ngroups << 4);
-  if (tid < rest) {
-    const int64_t i = (ngroups << 4) + tid;
-    Elem<DT>::store1(y, i, (float)(int32_t)codes[i] * scales[i >> lgB]);
+    for (int k = 0; k < E; ++k) v[k] = (float)(int32_t)(int8_t)(w[k >> 2] >> (8 * (k & 3))) * s;
+    store_elems<ZQ_NT_DEQ8, DT, E>(y, e0, v);
+  } else if (gid - ngroups < n - ngroups * E) {
+    const int64_t i = ngroups * E + (gid - ngroups);
+    store1<DT>(y, i, (float)(int32_t)codes[i] * scales[i >> lgB]);
   }
 }
 
 // ------------------------------------------------------------------ INT4 dequantise
-// A thread owns 16 consecutive nibbles (one 8-byte load).
 
 template <int DT>
 __global__ void __launch_bounds__(kThreads) k_qgz_dequant(const uint8_t* __restrict__ packed,
                                                           const float* __restrict__ scales, int64_t n, int lgB,
                                                           void* __restrict__ y) {
-  const int64_t ngroups = n >> 4;
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t nthreads = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t g = tid; g < ngroups; g += nthreads) {
-    const int64_t e0 = g << 4;
-    const uint2 w2 = *reinterpret_cast<const uint2*>(packed + (e0 >> 1));
-    const float s = scales[e0 >> lgB];
-    float v[16];
+  constexpr int E = deq4_elems(elem_size<DT>());
+  const int64_t ngroups = n / E;
+  const int64_t gid = group_index<false>() * blockDim.x + threadIdx.x;
+  if (gid < ngroups) {
+    const int64_t e0 = gid * E;
+    uint32_t w[E / 8];
+    load_words<ZQ_NT_DEQ4, E / 8>(packed + (e0 >> 1), w);
+    const float s = ld<ZQ_NT_DEQ4>(scales + (e0 >> lgB));
+    float v[E];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = nib_to_f32(w2.x, k) * s;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) v[8 + k] = nib_to_f32(w2.y, k) * s;
-    Elem<DT>::store16(y, e0, v);
-  }
-  const int64_t rest = n - (ngroups << 4);
-  if (tid < rest) {
-    const int64_t i = (ngroups << 4) + tid;
-    const uint32_t byte = packed[i >> 1];
-    Elem<DT>::store1(y, i, nib_to_f32(byte, (int)(i & 1)) * scales[i >> lgB]);
+    for (int k = 0; k < E; ++k) v[k] = nib_to_f32(w[k >> 3], k & 7) * s;
+    store_elems<ZQ_NT_DEQ4, DT, E>(y, e0, v);
+  } else if (gid - ngroups < n - ngroups * E) {
+    const int64_t i = ngroups * E + (gid - ngroups);
+    store1<DT>(y, i, nib_to_f32(packed[i >> 1], (int)(i & 1)) * scales[i >> lgB]);
   }
 }
 
 // ------------------------------------------------------------------ reduce level
 // Fast path: slices 16-byte aligned (m % 32 == 0), full blocks only.  A lane
-// owns 32 consecutive elements (16 bytes of every slice); L = B/32 lanes hold
-// one block.  Slices are summed in ascending order, exactly as defined.
+// owns 32 consecutive elements (16 bytes of every slice: consecutive lanes
+// read consecutive 16 B); L = B/32 lanes hold one block.
+//
+// Per slice and element: one v_cvt_off_f32_i4 (q/16), one multiply by 16*s
+// ((q/16)*(16 s) is the exact real q*s, so the rounded product is fl(q*s)),
+// one add.  16*s is exact unless it overflows (s > 2^123, i.e. inputs above
+// ~7e37); a wave holding such a scale multiplies by 16 first instead.  The
+// first slice initialises the sum with its product: +0 + x = x for every x
+// but -0, and a -0 sum and a +0 sum requantise to the same code and scale.
 
 template <int B>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
                                                      float* __restrict__ sout) {
-  constexpr int E = 32, L = B / E, BPW = 64 / L, U = 4;
+  constexpr int E = kReduceElems, L = B / E, BPW = 64 / L, U = ZQ_REDUCE_U;
+  static_assert(L >= 1 && L <= 64, "lane layout");
   const int lane = threadIdx.x & 63;
-  const int64_t ntiles = (nfull + BPW - 1) / BPW;
-  for (int64_t t = wave_id(); t < ntiles; t += wave_count()) {
-    const int64_t blk = t * BPW + lane / L;
-    const bool valid = blk < nfull;
-    const int64_t byte0 = (blk * B + (int64_t)(lane % L) * E) >> 1;
-    float acc[E];
+  const int64_t blk = wave_id() * BPW + lane / L;
+  const bool valid = blk < nfull;
+  const int64_t byte0 = (blk * B + (int64_t)(lane % L) * E) >> 1;
+  const uint8_t* src = in + byte0;
+  const float* ssrc = sin + blk;
+
+  float acc[E];
+  auto accumulate = [&](const u32x4& w4, float s, bool first) {
+    const float s16 = s * 16.0f;
+    const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
+    float prod[E];
+    if (__all(s16 <= kMaxFloat)) {  // wave-uniform: 16*s exact for every lane
 #pragma unroll
-    for (int k = 0; k < E; ++k) acc[k] = 0.0f;
-    for (int p0 = 0; p0 < P; p0 += U) {
-      uint4 w[U];
-      float s[U];
+      for (int j = 0; j < 4; ++j) {
+        nibbles_over_16(ww[j], prod + 8 * j);
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int p = p0 + u;
-        if (valid && p < P) {
-          w[u] = *reinterpret_cast<const uint4*>(in + (int64_t)p * slice_bytes + byte0);
-          s[u] = sin[(int64_t)p * slice_scales + blk];
-        } else {
-          w[u] = make_uint4(0u, 0u, 0u, 0u);
-          s[u] = 0.0f;
-        }
+        for (int k = 0; k < 8; ++k) prod[8 * j + k] = prod[8 * j + k] * s16;
       }
+    } else {
 #pragma unroll
-      for (int u = 0; u < U; ++u) {
-        if (p0 + u < P) {
-          const uint32_t ww[4] = {w[u].x, w[u].y, w[u].z, w[u].w};
+      for (int j = 0; j < 4; ++j) {
+        nibbles_over_16(ww[j], prod + 8 * j);
 #pragma unroll
-          for (int k = 0; k < E; ++k) {
-            const float prod = nib_to_f32(ww[k >> 3], k & 7) * s[u];
-            acc[k] = acc[k] + prod;
-          }
-        }
+        for (int k = 0; k < 8; ++k) prod[8 * j + k] = (prod[8 * j + k] * 16.0f) * s;
       }
     }
-    float a = fabsf(acc[0]);
 #pragma unroll
-    for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
-    const float amax = u2f(group_max<L>(f2u(a)));
-    float so = 0.0f, r = 0.0f;
-    if (amax >= kFlushBelow) {
-      so = amax / 7.0f;
-      r = 7.0f / amax;
-    }
-    uint32_t m[E];
+    for (int k = 0; k < E; ++k) acc[k] = first ? prod[k] : acc[k] + prod[k];
+  };
+
+  for (int p0 = 0; p0 < P; p0 += U) {
+    u32x4 w[U];
+    float s[U];
 #pragma unroll
-    for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
-    if (valid) {
-      *reinterpret_cast<uint4*>(out + byte0) =
-          make_uint4(pack_nibbles8(m), pack_nibbles8(m + 8), pack_nibbles8(m + 16), pack_nibbles8(m + 24));
-      if (lane % L == 0) sout[blk] = so;
+    for (int u = 0; u < U; ++u) {
+      const int p = p0 + u;
+      if (valid && p < P) {
+        w[u] = ld<ZQ_NT_REDUCE>(reinterpret_cast<const u32x4*>(src + (int64_t)p * slice_bytes));
+        s[u] = ld<ZQ_NT_REDUCE>(ssrc + (int64_t)p * slice_scales);
+      } else {
+        w[u] = u32x4{0u, 0u, 0u, 0u};
+        s[u] = 0.0f;
+      }
     }
+    if (p0 == 0) {
+      accumulate(w[0], s[0], true);
+    } else {
+      accumulate(w[0], s[0], false);
+    }
+#pragma unroll
+    for (int u = 1; u < U; ++u)
+      if (p0 + u < P) accumulate(w[u], s[u], false);
+  }
+
+  float a = fabsf(acc[0]);
+#pragma unroll
+  for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
+  const float amax = u2f(group_max<L>(f2u(a)));
+  float so = 0.0f, r = 0.0f;
+  if (amax >= kFlushBelow) {
+    so = amax / 7.0f;
+    r = 7.0f / amax;
+  }
+  uint32_t m[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
+  if (valid) {
+    st<ZQ_NT_REDUCE>(reinterpret_cast<u32x4*>(out + byte0),
+                     u32x4{pack_nibbles8(m), pack_nibbles8(m + 8), pack_nibbles8(m + 16), pack_nibbles8(m + 24)});
+    if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
   }
 }
 
 // Generic path: any m, any slice alignment; one wave per block, blocks
 // [blk_begin, blk_begin + gridDim.x).  A lane owns byte j = lane + 64 i of the
-// block (elements 2j, 2j+1), i < B/128 rounded up.
+// block (elements 2j, 2j+1), i < B/128 rounded up.  Plain arithmetic, the
+// definition as written: sum from +0, one multiply and one add per slice.
 __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                        int P, int64_t slice_bytes, int64_t slice_scales, int64_t m,
                                                        int B, int64_t blk_begin, uint8_t* __restrict__ out,
