@@ -22,8 +22,8 @@ constexpr int64_t kMaxGrid = 0x7fffffff;  // workgroups per launch
 
 // Workgroups to cover `units` at `units_per_wg` each (0 if it exceeds the
 // launch limit; callers turn that into ZQ_E_SIZE before anything is enqueued).
-int64_t grid_for(int64_t units, int64_t units_per_wg, bool remap = false) {
-  int64_t g = launch_grid((units + units_per_wg - 1) / units_per_wg, remap);
+int64_t grid_for(int64_t units, int64_t units_per_wg) {
+  int64_t g = (units + units_per_wg - 1) / units_per_wg;
   if (g < 1) g = 1;
   return g > kMaxGrid ? 0 : g;
 }
@@ -124,14 +124,11 @@ int dequantize(const void* codes, const float* scales, int64_t n, int32_t block,
   // thread g < n/E dequantises elements [gE, gE + E); the n % E leftovers go
   // to the following threads, one element each
   const int64_t E = qbits == 8 ? deq8_elems((int)elem_bytes(yt)) : deq4_elems((int)elem_bytes(yt));
-  const int64_t grid = grid_for(n / E + n % E, kThreads, qbits == 8 && ZQ_REMAP_DEQ8);
+  const int64_t grid = grid_for(n / E + n % E, kThreads);
   if (grid == 0) return ZQ_E_SIZE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (qbits == 8)
-    return launch(dequant8_kernel(yt), (unsigned)grid, kThreads, st, static_cast<const int8_t*>(codes), scales, n,
-                  lgB, y);
-  return launch(dequant4_kernel(yt), (unsigned)grid, kThreads, st, static_cast<const uint8_t*>(codes), scales, n,
-                lgB, y);
+  return launch(dequant_kernel(yt, qbits), (unsigned)grid, kThreads, st, static_cast<const uint8_t*>(codes), scales,
+                n, lgB, y);
 }
 
 }  // namespace
@@ -177,14 +174,16 @@ int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P
   // full blocks, 64 lanes x 32 elements per wave
   const bool vector_path = m % 32 == 0;
   const int64_t nfull = vector_path ? m / block : 0;
-  const int64_t blocks_per_wave = 64 / (block / kReduceElems);
+  const int64_t waves_large = (nfull + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
+  const bool small = block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES;
+  const int64_t blocks_per_wave = 64 / (block / (small ? kReduceElemsSmall : kReduceElems));
   const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64);
   if (grid == 0) return ZQ_E_SIZE;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (nfull > 0) {
-    int rc = launch(reduce_kernel(lgB), (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb,
-                    nfull, packed_out, scales_out);
+    int rc = launch(reduce_kernel(lgB, small), (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes,
+                    nb, nfull, packed_out, scales_out);
     if (rc != ZQ_OK) return rc;
   }
   const int64_t generic_from = nfull;

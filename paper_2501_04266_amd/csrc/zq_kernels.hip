@@ -45,14 +45,21 @@
 #ifndef ZQ_NT_REDUCE
 #define ZQ_NT_REDUCE 3
 #endif
+// Dequantisers with more than 16 output bytes per thread stage them in LDS.
+#ifndef ZQ_DEQ_STAGE
+#define ZQ_DEQ_STAGE 1
+#endif
 // Scale arrays are written 4 bytes per block, i.e. in partial cache lines:
 // plain stores let L2 merge them into full lines before write-back.
 #ifndef ZQ_NT_SCALES
 #define ZQ_NT_SCALES 0
 #endif
-// slices loaded ahead per batch in the reduce level
+// slices loaded ahead per batch in the reduce level (large / small levels)
 #ifndef ZQ_REDUCE_U
 #define ZQ_REDUCE_U 4
+#endif
+#ifndef ZQ_REDUCE_U_SMALL
+#define ZQ_REDUCE_U_SMALL 16
 #endif
 
 namespace zq {
@@ -85,6 +92,18 @@ __device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(flo
 __device__ __forceinline__ uint32_t code_bits(float v, float r) {
   float t = v * r;
   return f2u(t + kRoundMagic);
+}
+
+// Block scale fl(a / qmax) for a normal a >= 2^-119, via one binary64
+// multiply: a/qmax is either a binary32 value or lies at least
+// ulp(a/qmax) / (2 qmax) >= (a/qmax) * 2^-32 away from every binary32 rounding
+// boundary (qmax is odd, so a/qmax is not dyadic unless qmax divides a's
+// significand), while a * fl64(1/qmax) is within 2^-52 relative of a/qmax.
+// Rounding that to binary32 (nearest even) therefore gives fl(a / qmax),
+// the correctly rounded quotient, in 3 instructions instead of a division.
+template <int QMAX>
+__device__ __forceinline__ float scale_of(float amax) {
+  return (float)((double)amax * (1.0 / (double)QMAX));
 }
 
 // INT4 code (two's complement nibble k of w) as float.
@@ -254,33 +273,33 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
   else static_cast<uint16_t*>(p)[i] = (uint16_t)f2h(v);
 }
 
-// Logical workgroup index under the XCD remap (see zq_internal.h).  Indices
-// at or beyond `tiles` belong to padding workgroups, which do nothing.
-template <bool REMAP>
-__device__ __forceinline__ int64_t group_index() {
-  if constexpr (REMAP) {
-    const int64_t per = gridDim.x / kXcds;
-    return (int64_t)(blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
-  } else {
-    return blockIdx.x;
-  }
-}
-
 __device__ __forceinline__ int64_t wave_id() { return (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); }
 
 }  // namespace
 
 // ------------------------------------------------------------------ quantise
 // Full blocks only.  A lane owns E consecutive elements; L = B/E lanes hold
-// one block; one wave tile is 64/L blocks.
+// one block; one wave tile is 64/L blocks; a workgroup's tiles are adjacent,
+// so thread t's codes are bytes [t*OB, (t+1)*OB) of the workgroup's output.
+// The codes and scales of a workgroup are staged in LDS and written back as
+// one contiguous run of 16-byte stores: at this kernel's ~8:1 read:write mix
+// that keeps the write stream from slowing the reads (per-lane 2-byte stores
+// measured ~10% slower).  A workgroup holding the last, partial tile stores
+// straight from its lanes instead.
 
 template <int DT, int QBITS, int B>
 __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restrict__ x, int64_t nfull,
-                                                       uint8_t* __restrict__ out, float* __restrict__ scales) {
+                                                            uint8_t* __restrict__ out, float* __restrict__ scales) {
   constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
-  static_assert(E % 4 == 0 && L >= 1 && L <= 64, "lane layout");
-  const int lane = threadIdx.x & 63;
+  constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane
+  constexpr int WG_BLOCKS = kQuantThreads / 64 * BPW;           // blocks per workgroup
+  constexpr int WG_BYTES = kQuantThreads * OB;                  // code bytes per workgroup
+  static_assert(E % 4 == 0 && L >= 1 && L <= 64 && WG_BYTES % 16 == 0, "lane layout");
+  __shared__ u32x4 obuf[WG_BYTES / 16];
+  __shared__ float sbuf[WG_BLOCKS];
+
+  const int tid = threadIdx.x, lane = tid & 63;
   const int64_t blk = wave_id() * BPW + lane / L;
   const bool valid = blk < nfull;
   const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
@@ -297,26 +316,47 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   const float amax = u2f(group_max<L>(f2u(a)));
   float s = 0.0f, r = 0.0f;
   if (amax >= kFlushBelow) {
-    s = amax / QMAX;
+    s = scale_of<(int)QMAX>(amax);
     r = QMAX / amax;
   }
   uint32_t m[E];
 #pragma unroll
   for (int k = 0; k < E; ++k) m[k] = code_bits(v[k], r);
-  if (valid) {
-    if constexpr (QBITS == 8) {
-      uint32_t w[E / 4];
+
+  // this lane's packed codes: OB bytes, little-endian in w
+  constexpr int NWO = OB >= 4 ? OB / 4 : 1;
+  uint32_t w[NWO];
+  if constexpr (QBITS == 8) {
 #pragma unroll
-      for (int k = 0; k < E / 4; ++k) w[k] = pack_bytes4(m[4 * k], m[4 * k + 1], m[4 * k + 2], m[4 * k + 3]);
-      store_words<ZQ_NT_QUANT, E / 4>(out + e0, w);
-    } else if constexpr (E == 4) {
-      const uint32_t h = (m[0] & 0xfu) | ((m[1] & 0xfu) << 4) | ((m[2] & 0xfu) << 8) | ((m[3] & 0xfu) << 12);
-      st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(out + (e0 >> 1)), (uint16_t)h);
+    for (int k = 0; k < E / 4; ++k) w[k] = pack_bytes4(m[4 * k], m[4 * k + 1], m[4 * k + 2], m[4 * k + 3]);
+  } else if constexpr (E == 4) {
+    w[0] = (m[0] & 0xfu) | ((m[1] & 0xfu) << 4) | ((m[2] & 0xfu) << 8) | ((m[3] & 0xfu) << 12);
+  } else {
+#pragma unroll
+    for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
+  }
+
+  const int64_t wg_blk0 = (blk - lane / L) - (int64_t)(tid >> 6) * BPW;  // first block of the workgroup
+  if (wg_blk0 + WG_BLOCKS <= nfull) {  // workgroup-uniform
+    char* ob = reinterpret_cast<char*>(obuf) + tid * OB;
+    if constexpr (OB == 2) {
+      *reinterpret_cast<uint16_t*>(ob) = (uint16_t)w[0];
     } else {
-      uint32_t w[E / 8];
 #pragma unroll
-      for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
-      store_words<ZQ_NT_QUANT, E / 8>(out + (e0 >> 1), w);
+      for (int k = 0; k < NWO; ++k) reinterpret_cast<uint32_t*>(ob)[k] = w[k];
+    }
+    if (lane % L == 0) sbuf[(tid >> 6) * BPW + lane / L] = s;
+    __syncthreads();
+    u32x4* dst = reinterpret_cast<u32x4*>(out + (wg_blk0 * B * OB) / E);
+#pragma unroll
+    for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<ZQ_NT_QUANT>(dst + c, obuf[c]);
+    if (tid < WG_BLOCKS) st<2 * ZQ_NT_SCALES>(scales + wg_blk0 + tid, sbuf[tid]);
+  } else if (valid) {
+    uint8_t* dst = out + (e0 * OB) / E;
+    if constexpr (OB == 2) {
+      st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(dst), (uint16_t)w[0]);
+    } else {
+      store_words<ZQ_NT_QUANT, NWO>(dst, w);
     }
     if (lane % L == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
   }
@@ -333,7 +373,7 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
   const float amax = u2f(wave_max(f2u(a)));
   float s = 0.0f, r = 0.0f;
   if (amax >= kFlushBelow) {
-    s = amax / QMAX;
+    s = scale_of<(int)QMAX>(amax);
     r = QMAX / amax;
   }
   if constexpr (QBITS == 8) {
@@ -348,60 +388,74 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
   if (lane == 0) *scale = s;
 }
 
-// ------------------------------------------------------------------ INT8 dequantise
-// Thread g < n/E owns codes [gE, gE + E) (one block); the n % E leftover
-// elements go to the next threads, one each.
+// ------------------------------------------------------------------ dequantise
+// INT8 (QBITS 8) or INT4 (QBITS 4) codes -> binary32 products -> DT.  Thread g
+// < n/E owns elements [gE, gE + E) (one block, since E <= B); the n % E
+// leftover elements go to the following threads, one each.  When a thread's
+// output is wider than 16 bytes, a workgroup stages its outputs in LDS and
+// writes them back as wave-contiguous 16-byte stores (wide per-lane writes
+// lose bandwidth); the workgroup holding the end of the tensor stores
+// directly.
 
-template <int DT>
-__global__ void __launch_bounds__(kThreads) k_qwz_dequant(const int8_t* __restrict__ codes,
-                                                          const float* __restrict__ scales, int64_t n, int lgB,
-                                                          void* __restrict__ y) {
-  constexpr int E = deq8_elems(elem_size<DT>());
+template <int DT, int QBITS>
+__global__ void __launch_bounds__(kThreads) k_dequant(const uint8_t* __restrict__ codes,
+                                                      const float* __restrict__ scales, int64_t n, int lgB,
+                                                      void* __restrict__ y) {
+  constexpr int E = QBITS == 8 ? deq8_elems(elem_size<DT>()) : deq4_elems(elem_size<DT>());
+  constexpr int NT = QBITS == 8 ? ZQ_NT_DEQ8 : ZQ_NT_DEQ4;
+  constexpr int IB = QBITS == 8 ? E : E / 2;  // code bytes per thread
+  constexpr int OB = E * elem_size<DT>();     // output bytes per thread
+  constexpr bool STAGE = ZQ_DEQ_STAGE && OB > 16;
+  static_assert(IB % 4 == 0 && OB % 16 == 0, "lane layout");
+  __shared__ u32x4 ybuf[STAGE ? kThreads * OB / 16 : 1];
+
   const int64_t ngroups = n / E;
-  const int64_t gid = group_index<ZQ_REMAP_DEQ8 != 0>() * blockDim.x + threadIdx.x;
-  if (gid < ngroups) {
+  const int64_t g0 = (int64_t)blockIdx.x * kThreads;
+  const int64_t gid = g0 + threadIdx.x;
+  if (STAGE && g0 + kThreads <= ngroups) {  // workgroup-uniform
     const int64_t e0 = gid * E;
-    uint32_t w[E / 4];
-    load_words<ZQ_NT_DEQ8, E / 4>(codes + e0, w);
-    const float s = ld<ZQ_NT_DEQ8>(scales + (e0 >> lgB));
+    uint32_t w[IB / 4];
+    load_words<NT, IB / 4>(codes + (e0 * IB) / E, w);
+    const float s = ld<NT>(scales + (e0 >> lgB));
     float v[E];
 #pragma unroll
-    for (int k = 0; k < E; ++k) v[k] = (float)(int32_t)(int8_t)(w[k >> 2] >> (8 * (k & 3))) * s;
-    store_elems<ZQ_NT_DEQ8, DT, E>(y, e0, v);
-  } else if (gid - ngroups < n - ngroups * E) {
-    const int64_t i = ngroups * E + (gid - ngroups);
-    store1<DT>(y, i, (float)(int32_t)codes[i] * scales[i >> lgB]);
-  }
-}
-
-// ------------------------------------------------------------------ INT4 dequantise
-
-template <int DT>
-__global__ void __launch_bounds__(kThreads) k_qgz_dequant(const uint8_t* __restrict__ packed,
-                                                          const float* __restrict__ scales, int64_t n, int lgB,
-                                                          void* __restrict__ y) {
-  constexpr int E = deq4_elems(elem_size<DT>());
-  const int64_t ngroups = n / E;
-  const int64_t gid = group_index<false>() * blockDim.x + threadIdx.x;
-  if (gid < ngroups) {
+    for (int k = 0; k < E; ++k) {
+      if constexpr (QBITS == 8) v[k] = (float)(int32_t)(int8_t)(w[k >> 2] >> (8 * (k & 3))) * s;
+      else v[k] = nib_to_f32(w[k >> 3], k & 7) * s;
+    }
+    store_elems<0, DT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * OB, 0, v);
+    __syncthreads();
+    u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + g0 * OB);
+#pragma unroll
+    for (int c = 0; c < OB / 16; ++c) st<NT>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
+  } else if (gid < ngroups) {
     const int64_t e0 = gid * E;
-    uint32_t w[E / 8];
-    load_words<ZQ_NT_DEQ4, E / 8>(packed + (e0 >> 1), w);
-    const float s = ld<ZQ_NT_DEQ4>(scales + (e0 >> lgB));
+    uint32_t w[IB / 4];
+    load_words<NT, IB / 4>(codes + (e0 * IB) / E, w);
+    const float s = ld<NT>(scales + (e0 >> lgB));
     float v[E];
 #pragma unroll
-    for (int k = 0; k < E; ++k) v[k] = nib_to_f32(w[k >> 3], k & 7) * s;
-    store_elems<ZQ_NT_DEQ4, DT, E>(y, e0, v);
+    for (int k = 0; k < E; ++k) {
+      if constexpr (QBITS == 8) v[k] = (float)(int32_t)(int8_t)(w[k >> 2] >> (8 * (k & 3))) * s;
+      else v[k] = nib_to_f32(w[k >> 3], k & 7) * s;
+    }
+    store_elems<NT, DT, E>(y, e0, v);
   } else if (gid - ngroups < n - ngroups * E) {
     const int64_t i = ngroups * E + (gid - ngroups);
-    store1<DT>(y, i, nib_to_f32(packed[i >> 1], (int)(i & 1)) * scales[i >> lgB]);
+    float prod;
+    if constexpr (QBITS == 8) prod = (float)(int32_t)(int8_t)codes[i] * scales[i >> lgB];
+    else prod = nib_to_f32(codes[i >> 1], (int)(i & 1)) * scales[i >> lgB];
+    store1<DT>(y, i, prod);
   }
 }
 
 // ------------------------------------------------------------------ reduce level
-// Fast path: slices 16-byte aligned (m % 32 == 0), full blocks only.  A lane
-// owns 32 consecutive elements (16 bytes of every slice: consecutive lanes
-// read consecutive 16 B); L = B/32 lanes hold one block.
+// Vector path: slices 16-byte aligned (m % 32 == 0), full blocks only.  A lane
+// owns E consecutive elements (E/2 bytes of every slice: consecutive lanes
+// read consecutive bytes); L = B/E lanes hold one block.  Large levels use
+// E = 32 (16 B per slice per lane) with U = 4 slices loaded ahead; small levels
+// (few waves, often many slices) use E = 8 with U = 16, so four times as many
+// waves run and each has 16 slices in flight instead of 4.
 //
 // Per slice and element: one v_cvt_off_f32_i4 (q/16), one multiply by 16*s
 // ((q/16)*(16 s) is the exact real q*s, so the rounded product is fl(q*s)),
@@ -409,14 +463,15 @@ __global__ void __launch_bounds__(kThreads) k_qgz_dequant(const uint8_t* __restr
 // ~7e37); a wave holding such a scale multiplies by 16 first instead.  The
 // first slice initialises the sum with its product: +0 + x = x for every x
 // but -0, and a -0 sum and a +0 sum requantise to the same code and scale.
+// Slices are summed in ascending order, exactly as defined.
 
-template <int B>
+template <int B, int E, int U>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
                                                      float* __restrict__ sout) {
-  constexpr int E = kReduceElems, L = B / E, BPW = 64 / L, U = ZQ_REDUCE_U;
-  static_assert(L >= 1 && L <= 64, "lane layout");
+  constexpr int L = B / E, BPW = 64 / L, NW = E / 8;  // NW words of nibbles per slice per lane
+  static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4), "lane layout");
   const int lane = threadIdx.x & 63;
   const int64_t blk = wave_id() * BPW + lane / L;
   const bool valid = blk < nfull;
@@ -425,40 +480,46 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   const float* ssrc = sin + blk;
 
   float acc[E];
-  auto accumulate = [&](const u32x4& w4, float s, bool first) {
+  // one slice into the sum, word by word (8 products live at a time)
+  auto accumulate = [&](const uint32_t (&ww)[NW], float s, bool first) {
     const float s16 = s * 16.0f;
-    const uint32_t ww[4] = {w4.x, w4.y, w4.z, w4.w};
-    float prod[E];
     if (__all(s16 <= kMaxFloat)) {  // wave-uniform: 16*s exact for every lane
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        nibbles_over_16(ww[j], prod + 8 * j);
+      for (int j = 0; j < NW; ++j) {
+        float f[8];
+        nibbles_over_16(ww[j], f);
 #pragma unroll
-        for (int k = 0; k < 8; ++k) prod[8 * j + k] = prod[8 * j + k] * s16;
+        for (int k = 0; k < 8; ++k) {
+          const float prod = f[k] * s16;
+          acc[8 * j + k] = first ? prod : acc[8 * j + k] + prod;
+        }
       }
     } else {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        nibbles_over_16(ww[j], prod + 8 * j);
+      for (int j = 0; j < NW; ++j) {
+        float f[8];
+        nibbles_over_16(ww[j], f);
 #pragma unroll
-        for (int k = 0; k < 8; ++k) prod[8 * j + k] = (prod[8 * j + k] * 16.0f) * s;
+        for (int k = 0; k < 8; ++k) {
+          const float prod = (f[k] * 16.0f) * s;
+          acc[8 * j + k] = first ? prod : acc[8 * j + k] + prod;
+        }
       }
     }
-#pragma unroll
-    for (int k = 0; k < E; ++k) acc[k] = first ? prod[k] : acc[k] + prod[k];
   };
 
   for (int p0 = 0; p0 < P; p0 += U) {
-    u32x4 w[U];
+    uint32_t w[U][NW];
     float s[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int p = p0 + u;
       if (valid && p < P) {
-        w[u] = ld<ZQ_NT_REDUCE>(reinterpret_cast<const u32x4*>(src + (int64_t)p * slice_bytes));
+        load_words<ZQ_NT_REDUCE, NW>(src + (int64_t)p * slice_bytes, w[u]);
         s[u] = ld<ZQ_NT_REDUCE>(ssrc + (int64_t)p * slice_scales);
       } else {
-        w[u] = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int j = 0; j < NW; ++j) w[u][j] = 0u;
         s[u] = 0.0f;
       }
     }
@@ -478,15 +539,17 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   const float amax = u2f(group_max<L>(f2u(a)));
   float so = 0.0f, r = 0.0f;
   if (amax >= kFlushBelow) {
-    so = amax / 7.0f;
+    so = scale_of<7>(amax);
     r = 7.0f / amax;
   }
   uint32_t m[E];
 #pragma unroll
   for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
   if (valid) {
-    st<ZQ_NT_REDUCE>(reinterpret_cast<u32x4*>(out + byte0),
-                     u32x4{pack_nibbles8(m), pack_nibbles8(m + 8), pack_nibbles8(m + 16), pack_nibbles8(m + 24)});
+    uint32_t o[NW];
+#pragma unroll
+    for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
+    store_words<ZQ_NT_REDUCE, NW>(out + byte0, o);
     if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
   }
 }
@@ -533,7 +596,7 @@ __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict
   const float amax = u2f(wave_max(f2u(a)));
   float so = 0.0f, r = 0.0f;
   if (amax >= kFlushBelow) {
-    so = amax / 7.0f;
+    so = scale_of<7>(amax);
     r = 7.0f / amax;
   }
 #pragma unroll
@@ -584,26 +647,26 @@ QuantTailKernel quant_tail_kernel(int dt, int qbits) {
   return &k_quantize_tail<ZQ_BF16, 4>;
 }
 
-Dequant8Kernel dequant8_kernel(int dt) {
-  if (dt == ZQ_F32) return &k_qwz_dequant<ZQ_F32>;
-  if (dt == ZQ_F16) return &k_qwz_dequant<ZQ_F16>;
-  return &k_qwz_dequant<ZQ_BF16>;
+DequantKernel dequant_kernel(int dt, int qbits) {
+  if (qbits == 8) {
+    if (dt == ZQ_F32) return &k_dequant<ZQ_F32, 8>;
+    if (dt == ZQ_F16) return &k_dequant<ZQ_F16, 8>;
+    return &k_dequant<ZQ_BF16, 8>;
+  }
+  if (dt == ZQ_F32) return &k_dequant<ZQ_F32, 4>;
+  if (dt == ZQ_F16) return &k_dequant<ZQ_F16, 4>;
+  return &k_dequant<ZQ_BF16, 4>;
 }
 
-Dequant4Kernel dequant4_kernel(int dt) {
-  if (dt == ZQ_F32) return &k_qgz_dequant<ZQ_F32>;
-  if (dt == ZQ_F16) return &k_qgz_dequant<ZQ_F16>;
-  return &k_qgz_dequant<ZQ_BF16>;
-}
-
-ReduceKernel reduce_kernel(int lgB) {
+ReduceKernel reduce_kernel(int lgB, bool small) {
+  constexpr int EL = kReduceElems, UL = ZQ_REDUCE_U, ES = kReduceElemsSmall, US = ZQ_REDUCE_U_SMALL;
   switch (lgB) {
-    case 5: return &k_reduce<32>;
-    case 6: return &k_reduce<64>;
-    case 7: return &k_reduce<128>;
-    case 8: return &k_reduce<256>;
-    case 9: return &k_reduce<512>;
-    default: return &k_reduce<1024>;
+    case 5: return small ? &k_reduce<32, ES, US> : &k_reduce<32, EL, UL>;
+    case 6: return small ? &k_reduce<64, ES, US> : &k_reduce<64, EL, UL>;
+    case 7: return small ? &k_reduce<128, ES, US> : &k_reduce<128, EL, UL>;
+    case 8: return small ? &k_reduce<256, ES, US> : &k_reduce<256, EL, UL>;
+    case 9: return small ? &k_reduce<512, ES, US> : &k_reduce<512, EL, UL>;
+    default: return &k_reduce<1024, EL, UL>;  // a block may span at most one wave
   }
 }
 
