@@ -46,10 +46,6 @@ def nb4(n):
 
 
 # algorithmic bytes per call (what the method must read and write)
-def bytes_quant(n, in_b, out_b_per_elem, block):
-    return n * in_b + int(n * out_b_per_elem) + 4 * nsc(n, block)
-
-
 def bytes_qwz_quant(n, in_b, block):
     return n * in_b + n + 4 * nsc(n, block)
 
@@ -188,10 +184,11 @@ class Layer20B:
         mark(i + 1)
 
 
-def oracle_step(L, threads):
+def oracle_step(L, threads, repeats=1):
     """The same step on the CPU oracle over the same host inputs; returns
-    (seconds in the timed calls, outputs).  Preparation (gathered codes, peer
-    slices) is untimed, as on the GPU."""
+    (mean seconds per step in the timed calls, outputs).  Each timed call runs
+    `repeats` times.  Preparation (gathered codes, peer slices) is untimed, as
+    on the GPU."""
     import numpy as np
 
     import oracle
@@ -204,8 +201,9 @@ def oracle_step(L, threads):
     def timed(fn, *a):
         nonlocal t
         t0 = time.perf_counter()
-        r = fn(*a)
-        t += time.perf_counter() - t0
+        for _ in range(repeats):
+            r = fn(*a)
+        t += (time.perf_counter() - t0) / repeats
         return r
 
     outs["shard_codes"] = timed(oracle.qwz_quantize, w[:s], WBLOCK, "bf16")
@@ -262,20 +260,32 @@ def check_against_oracle(L, outs):
     return bad
 
 
-def load_traffic(kernel_name):
-    """HBM bytes per launch from committed rocprofv3 PMC summaries, if they
-    were taken on the current kernel source."""
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2501_04266_amd", "csrc", f)
+                  for f in ("zq_kernels.hip", "zq_internal.h", "zq_api.hip")]
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_pmc_traffic.txt")
+
+
+def kernel_source_hash():
     import hashlib
-    path = os.path.join(ROOT, "profiles", "pmc_traffic.json")
-    if not os.path.exists(path):
+    return hashlib.sha256(b"".join(open(p, "rb").read() for p in KERNEL_SOURCES)).hexdigest()[:16]
+
+
+def load_traffic(call):
+    """HBM bytes per launch of `call` from the committed rocprofv3 PMC summary
+    (FETCH_SIZE and WRITE_SIZE runs, calibrated on a plain copy), or None when
+    there is none or it was taken on different kernel sources."""
+    if not os.path.exists(TRAFFIC_PROFILE):
         return None
-    d = json.load(open(path))
-    src = os.path.join(ROOT, "paper_2501_04266_amd", "csrc", "zq_kernels.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if d.get("kernel_source_sha256_16") != h:
+    lines = open(TRAFFIC_PROFILE).read().splitlines()
+    tag = "# kernel source sha256[:16]:"
+    h = next((ln[len(tag):].strip() for ln in lines if ln.startswith(tag)), None)
+    if h != kernel_source_hash():
         return None
-    ent = d.get("kernels", {}).get(kernel_name)
-    return ent.get("bytes_per_launch") if ent else None
+    for ln in lines:
+        if ln.startswith(call + " ") and not ln.startswith("#"):
+            rest = ln[len(call):].split()
+            return int(rest[2])
+    return None
 
 
 def main():
@@ -285,6 +295,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
+    ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
     ap.add_argument("--n", type=int, default=0, help=argparse.SUPPRESS)  # smaller layer for quick checks
     args = ap.parse_args()
 
@@ -374,11 +385,12 @@ def main():
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or max(1, len(os.sched_getaffinity(0)))
         log(f"oracle step on {threads} threads ...")
-        secs, outs = oracle_step(L, threads)
+        secs, outs = oracle_step(L, threads, args.cpu_repeats)
         bad = check_against_oracle(L, outs)
         out["cpu_baseline"] = {"value": round(step_bytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
-                               "kind": "oracle", "seconds": round(secs, 2),
-                               "sample": "one full step of the same workload (all calls, full sizes)"}
+                               "kind": "oracle", "seconds_per_step": round(secs, 3),
+                               "sample": f"the full step of the same workload (all calls, full sizes), each timed "
+                                         f"call repeated {args.cpu_repeats}x, mean"}
         out["parity"] = "bit-exact vs oracle (all step outputs)" if not bad else f"MISMATCH: {bad}"
         log(f"oracle {secs:.1f}s; parity: {out['parity']}")
     print(json.dumps(out), flush=True)
