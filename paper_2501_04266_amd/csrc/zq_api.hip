@@ -124,11 +124,11 @@ int dequantize(const void* codes, const float* scales, int64_t n, int32_t block,
   // thread g < n/E dequantises elements [gE, gE + E); the n % E leftovers go
   // to the following threads, one element each
   const int64_t E = qbits == 8 ? deq8_elems((int)elem_bytes(yt)) : deq4_elems((int)elem_bytes(yt));
-  const int64_t grid = grid_for(n / E + n % E, kThreads);
+  const int64_t grid = grid_for(n / E + n % E, kDeqThreads);
   if (grid == 0) return ZQ_E_SIZE;
   hipStream_t st = static_cast<hipStream_t>(stream);
-  return launch(dequant_kernel(yt, qbits), (unsigned)grid, kThreads, st, static_cast<const uint8_t*>(codes), scales,
-                n, lgB, y);
+  return launch(dequant_kernel(yt, qbits), (unsigned)grid, kDeqThreads, st, static_cast<const uint8_t*>(codes),
+                scales, n, lgB, y);
 }
 
 }  // namespace

@@ -10,6 +10,10 @@ constexpr int kThreads = 256;  // threads per workgroup of the streaming kernels
 #define ZQ_QUANT_THREADS 256
 #endif
 constexpr int kQuantThreads = ZQ_QUANT_THREADS;
+#ifndef ZQ_DEQ_THREADS
+#define ZQ_DEQ_THREADS 256
+#endif
+constexpr int kDeqThreads = ZQ_DEQ_THREADS;
 
 
 // Elements per lane.  Each wave handles one tile of 64 lanes x E elements and

@@ -398,7 +398,7 @@ __global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x
 // directly.
 
 template <int DT, int QBITS>
-__global__ void __launch_bounds__(kThreads) k_dequant(const uint8_t* __restrict__ codes,
+__global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restrict__ codes,
                                                       const float* __restrict__ scales, int64_t n, int lgB,
                                                       void* __restrict__ y) {
   constexpr int E = QBITS == 8 ? deq8_elems(elem_size<DT>()) : deq4_elems(elem_size<DT>());
@@ -407,12 +407,12 @@ __global__ void __launch_bounds__(kThreads) k_dequant(const uint8_t* __restrict_
   constexpr int OB = E * elem_size<DT>();     // output bytes per thread
   constexpr bool STAGE = ZQ_DEQ_STAGE && OB > 16;
   static_assert(IB % 4 == 0 && OB % 16 == 0, "lane layout");
-  __shared__ u32x4 ybuf[STAGE ? kThreads * OB / 16 : 1];
+  __shared__ u32x4 ybuf[STAGE ? kDeqThreads * OB / 16 : 1];
 
   const int64_t ngroups = n / E;
-  const int64_t g0 = (int64_t)blockIdx.x * kThreads;
+  const int64_t g0 = (int64_t)blockIdx.x * kDeqThreads;
   const int64_t gid = g0 + threadIdx.x;
-  if (STAGE && g0 + kThreads <= ngroups) {  // workgroup-uniform
+  if (STAGE && g0 + kDeqThreads <= ngroups) {  // workgroup-uniform
     const int64_t e0 = gid * E;
     uint32_t w[IB / 4];
     load_words<NT, IB / 4>(codes + (e0 * IB) / E, w);
@@ -427,7 +427,7 @@ __global__ void __launch_bounds__(kThreads) k_dequant(const uint8_t* __restrict_
     __syncthreads();
     u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + g0 * OB);
 #pragma unroll
-    for (int c = 0; c < OB / 16; ++c) st<NT>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
+    for (int c = 0; c < OB / 16; ++c) st<NT>(dst + c * kDeqThreads + threadIdx.x, ybuf[c * kDeqThreads + threadIdx.x]);
   } else if (gid < ngroups) {
     const int64_t e0 = gid * E;
     uint32_t w[IB / 4];
