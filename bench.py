@@ -352,6 +352,34 @@ def main():
     achieved = dom_bytes / (per_call_ms[dom] * 1e-3) / 1e9
     traffic = load_traffic(dom_name)
 
+    # next row: the last level fused with the final dequantisation, against the
+    # two separate calls it replaces (same inputs, same outputs bit for bit)
+    fused = {}
+    for label, (P, m, d, o), yout in (("P=8 level + dequant", (8, L.m8, L.d8, L.o8), L.gshard),
+                                      ("P=48 level + dequant", L.chain[-1], L.final)):
+        def separate():
+            zq.qgz_reduce_level(d[0], d[1], P, m, GBLOCK, packed_out=o[0], scales_out=o[1])
+            zq.qgz_dequantize(o[0], o[1], m, GBLOCK, y=yout)
+
+        def fused_call():
+            zq.qgz_reduce_dequantize(d[0], d[1], P, m, GBLOCK, y=yout)
+
+        times = {}
+        for name, fn in (("separate", separate), ("fused", fused_call)):
+            for _ in range(3):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(args.steps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            times[name] = e0.elapsed_time(e1) * 1e3 / args.steps
+        fused_bytes = P * (nb4(m) + 4 * nsc(m, GBLOCK)) + 4 * m
+        fused[label] = {"separate_us": round(times["separate"], 2), "fused_us": round(times["fused"], 2),
+                        "fused_bytes": fused_bytes,
+                        "fused_GBps": round(fused_bytes / (times["fused"] * 1e-6) / 1e9, 1)}
+
     # practical ceiling: a plain device-to-device copy of 1 GiB
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
@@ -379,6 +407,7 @@ def main():
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "us_per_launch": round(per_call_ms[dom] * 1e3, 2)},
         "kernels": kernels,
+        "fused_last_level": fused,
         "copy_ceiling_GBps": round(copy_gbps, 1),
     }
 

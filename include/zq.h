@@ -115,6 +115,18 @@ int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P
 int qgz_dequantize(const uint8_t* packed, const float* scales, int64_t n, int32_t block,
                    void* y, zq_dtype yt, void* stream);
 
+/* Fused last level: the receiver's final reduce level followed by the
+ * dequantisation of the resulting gradient shard for the optimizer (Design,
+ * Gradient Partitioning; Background, ZeRO++: quantised reduce-scatter).
+ * Writes y [m] of dtype yt, bit-identical to qgz_dequantize applied to what
+ * qgz_reduce_level would produce from the same slices, without storing and
+ * re-reading the INT4 result.  packed_out / scales_out are optional: both NULL,
+ * or both given to receive that INT4 result as well.  Slice layout, limits
+ * and errors as qgz_reduce_level; y must be 16-byte aligned and overlap no
+ * input or output. */
+int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
+                          void* y, zq_dtype yt, uint8_t* packed_out, float* scales_out, void* stream);
+
 /* Size helpers (host only): number of scales ceil(n/block) (-1 on a bad
  * block or n < 0), and INT4 bytes ceil(n/2) (-1 for n < 0). */
 int64_t zq_num_scales(int64_t n, int32_t block);

@@ -15,6 +15,7 @@ from ._lib import (  # noqa: F401
     num_scales,
     qgz_dequantize,
     qgz_quantize,
+    qgz_reduce_dequantize,
     qgz_reduce_level,
     qwz_dequantize,
     qwz_quantize,

@@ -17,7 +17,7 @@ ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
 STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",
           -5: "ZQ_E_SIZE", -6: "ZQ_E_P", -7: "ZQ_E_HIP", -8: "ZQ_E_ALIAS"}
 EXPORTS = ["qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-           "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
+           "qgz_reduce_dequantize", "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
 
 _TORCH_DT = {torch.float32: ZQ_F32, torch.float16: ZQ_F16, torch.bfloat16: ZQ_BF16}
 _DT_TORCH = {v: k for k, v in _TORCH_DT.items()}
@@ -45,6 +45,7 @@ def lib():
         "qgz_quantize": [vp, ci, i64, i32, vp, vp, vp],
         "qgz_dequantize": [vp, vp, i64, i32, vp, ci, vp],
         "qgz_reduce_level": [vp, vp, i32, i64, i32, vp, vp, vp],
+        "qgz_reduce_dequantize": [vp, vp, i32, i64, i32, vp, ci, vp, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -138,3 +139,22 @@ def qgz_reduce_level(packed_in, scales_in, P, m, block=128, packed_out=None, sca
                                   _dev(packed_out, "packed_out"), _dev(scales_out, "scales_out"),
                                   _stream(stream)), "qgz_reduce_level")
     return packed_out, scales_out
+
+
+def qgz_reduce_dequantize(packed_in, scales_in, P, m, block=128, out_dtype=torch.float32, y=None,
+                          packed_out=None, scales_out=None, stream=None):
+    """Last level fused with the final dequantisation: returns y (m elements of
+    out_dtype) bit-identical to qgz_dequantize(qgz_reduce_level(...)).  Pass
+    packed_out and scales_out to also receive the INT4 result."""
+    if y is None:
+        y = torch.empty(m, dtype=out_dtype, device=packed_in.device)
+    if (packed_out is None) != (scales_out is None):
+        raise ValueError("give both packed_out and scales_out, or neither")
+    if packed_in.numel() < P * int4_bytes(m) or scales_in.numel() < P * num_scales(m, block):
+        raise ValueError("slice buffers smaller than P slices of m elements")
+    _check(lib().qgz_reduce_dequantize(_dev(packed_in, "packed_in"), _dev(scales_in, "scales_in"), P, m, block,
+                                       _dev(y, "y"), _TORCH_DT[y.dtype],
+                                       None if packed_out is None else _dev(packed_out, "packed_out"),
+                                       None if scales_out is None else _dev(scales_out, "scales_out"),
+                                       _stream(stream)), "qgz_reduce_dequantize")
+    return y

@@ -131,6 +131,65 @@ int dequantize(const void* codes, const float* scales, int64_t n, int32_t block,
                 scales, n, lgB, y);
 }
 
+// Shared body of qgz_reduce_level (fused = false: INT4 output only, both
+// pointers required) and qgz_reduce_dequantize (fused = true: y of dtype yt
+// required, the INT4 output optional -- both of its pointers or neither).
+int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
+           uint8_t* packed_out, float* scales_out, bool fused, void* y, int yt, void* stream) {
+  if (m < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (fused && !dtype_ok(yt)) return ZQ_E_DTYPE;
+  if (P < 1 || P > 1024) return ZQ_E_P;
+  if (m == 0) return ZQ_OK;
+  if (!packed_in || !scales_in || (packed_out == nullptr) != (scales_out == nullptr)) return ZQ_E_NULL;
+  if (fused ? y == nullptr : packed_out == nullptr) return ZQ_E_NULL;
+  if (!aligned(packed_in, 16) || !aligned(scales_in, 4)) return ZQ_E_ALIGN;
+  if (packed_out && (!aligned(packed_out, 16) || !aligned(scales_out, 4))) return ZQ_E_ALIGN;
+  if (fused && !aligned(y, 16)) return ZQ_E_ALIGN;
+  const int64_t slice_bytes = (m + 1) / 2, nb = num_scales(m, block);
+  const Range ins[] = {{packed_in, slice_bytes * P}, {scales_in, 4 * nb * P}};
+  Range outs[3];
+  int nouts = 0;
+  if (packed_out) {
+    outs[nouts++] = {packed_out, slice_bytes};
+    outs[nouts++] = {scales_out, 4 * nb};
+  }
+  if (fused) outs[nouts++] = {y, m * elem_bytes(yt)};
+  for (int o = 0; o < nouts; ++o) {
+    for (const Range& in : ins)
+      if (overlap(outs[o], in)) return ZQ_E_ALIAS;
+    for (int o2 = o + 1; o2 < nouts; ++o2)
+      if (overlap(outs[o], outs[o2])) return ZQ_E_ALIAS;
+  }
+
+  // every slice starts 16-byte aligned when m % 32 == 0: vector path over the
+  // full blocks, 64 lanes x E elements per wave
+  const bool vector_path = m % 32 == 0;
+  const int64_t nfull = vector_path ? m / block : 0;
+  const int64_t waves_large = (nfull + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
+  const bool small = block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES;
+  const int64_t blocks_per_wave = 64 / (block / (small ? kReduceElemsSmall : kReduceElems));
+  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64);
+  if (grid == 0) return ZQ_E_SIZE;
+
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (nfull > 0) {
+    int rc = launch(reduce_kernel(lgB, small, fused ? yt : -1), (unsigned)grid, kThreads, st, packed_in, scales_in,
+                    (int)P, slice_bytes, nb, nfull, packed_out, scales_out, y);
+    if (rc != ZQ_OK) return rc;
+  }
+  // remaining blocks (a short last block, or all of them when slices are not
+  // 16-byte aligned): one wave per block
+  for (int64_t b0 = nfull; b0 < nb; b0 += (1LL << 30)) {
+    const int64_t cnt = (nb - b0) < (1LL << 30) ? (nb - b0) : (1LL << 30);
+    int rc = launch(reduce_generic_kernel(), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes, nb, m,
+                    (int)block, b0, packed_out, scales_out, fused ? y : nullptr, fused ? yt : 0);
+    if (rc != ZQ_OK) return rc;
+  }
+  return ZQ_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -157,45 +216,12 @@ int qgz_dequantize(const uint8_t* packed, const float* scales, int64_t n, int32_
 
 int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
                      uint8_t* packed_out, float* scales_out, void* stream) {
-  if (m < 0) return ZQ_E_SIZE;
-  const int lgB = log2_block(block);
-  if (lgB < 0) return ZQ_E_BLOCK;
-  if (P < 1 || P > 1024) return ZQ_E_P;
-  if (m == 0) return ZQ_OK;
-  if (!packed_in || !scales_in || !packed_out || !scales_out) return ZQ_E_NULL;
-  if (!aligned(packed_in, 16) || !aligned(packed_out, 16) || !aligned(scales_in, 4) || !aligned(scales_out, 4))
-    return ZQ_E_ALIGN;
-  const int64_t slice_bytes = (m + 1) / 2, nb = num_scales(m, block);
-  if (any_overlap({{packed_out, slice_bytes}, {scales_out, 4 * nb}},
-                  {{packed_in, slice_bytes * P}, {scales_in, 4 * nb * P}}))
-    return ZQ_E_ALIAS;
+  return reduce(packed_in, scales_in, P, m, block, packed_out, scales_out, false, nullptr, -1, stream);
+}
 
-  // every slice starts 16-byte aligned when m % 32 == 0: vector path over the
-  // full blocks, 64 lanes x 32 elements per wave
-  const bool vector_path = m % 32 == 0;
-  const int64_t nfull = vector_path ? m / block : 0;
-  const int64_t waves_large = (nfull + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
-  const bool small = block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES;
-  const int64_t blocks_per_wave = 64 / (block / (small ? kReduceElemsSmall : kReduceElems));
-  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64);
-  if (grid == 0) return ZQ_E_SIZE;
-
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  if (nfull > 0) {
-    int rc = launch(reduce_kernel(lgB, small), (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes,
-                    nb, nfull, packed_out, scales_out);
-    if (rc != ZQ_OK) return rc;
-  }
-  const int64_t generic_from = nfull;
-  // remaining blocks (a short last block, or all of them when slices are not
-  // 16-byte aligned): one wave per block
-  for (int64_t b0 = generic_from; b0 < nb; b0 += (1LL << 30)) {
-    const int64_t cnt = (nb - b0) < (1LL << 30) ? (nb - b0) : (1LL << 30);
-    int rc = launch(reduce_generic_kernel(), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes, nb, m,
-                    (int)block, b0, packed_out, scales_out);
-    if (rc != ZQ_OK) return rc;
-  }
-  return ZQ_OK;
+int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
+                          void* y, zq_dtype yt, uint8_t* packed_out, float* scales_out, void* stream) {
+  return reduce(packed_in, scales_in, P, m, block, packed_out, scales_out, true, y, yt, stream);
 }
 
 int64_t zq_num_scales(int64_t n, int32_t block) {

@@ -59,14 +59,15 @@ constexpr int kReduceElemsSmall = 8;  // 4 bytes per slice per lane, for small l
 using QuantKernel = void (*)(const void*, int64_t, uint8_t*, float*);
 using QuantTailKernel = void (*)(const void*, int64_t, int, uint8_t*, float*);
 using DequantKernel = void (*)(const uint8_t*, const float*, int64_t, int, void*);
-using ReduceKernel = void (*)(const uint8_t*, const float*, int, int64_t, int64_t, int64_t, uint8_t*, float*);
+using ReduceKernel = void (*)(const uint8_t*, const float*, int, int64_t, int64_t, int64_t, uint8_t*, float*, void*);
 using ReduceGenericKernel = void (*)(const uint8_t*, const float*, int, int64_t, int64_t, int64_t, int, int64_t,
-                                     uint8_t*, float*);
+                                     uint8_t*, float*, void*, int);
 
 QuantKernel quant_kernel(int dt, int qbits, int lgB);
 QuantTailKernel quant_tail_kernel(int dt, int qbits);
 DequantKernel dequant_kernel(int dt, int qbits);
-ReduceKernel reduce_kernel(int lgB, bool small);
+// ydt < 0: INT4 output only; otherwise also the fused dequantisation to ydt
+ReduceKernel reduce_kernel(int lgB, bool small, int ydt);
 ReduceGenericKernel reduce_generic_kernel();
 
 }  // namespace zq

@@ -465,17 +465,28 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
 // but -0, and a -0 sum and a +0 sum requantise to the same code and scale.
 // Slices are summed in ascending order, exactly as defined.
 
-template <int B, int E, int U>
+// YDT >= 0 adds the fused final dequantisation: the requantised codes are
+// turned back into fl(code * s_out) in YDT (the value qgz_dequantize would
+// produce from this level's output) and written to y; out / sout may then be
+// null, in which case the INT4 result is not stored.  Outputs wider than 16
+// bytes per lane are staged in LDS and written as wave-contiguous 16-byte
+// stores, as in the dequantiser.
+
+template <int B, int E, int U, int YDT>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
-                                                     float* __restrict__ sout) {
+                                                     float* __restrict__ sout, void* __restrict__ y) {
   constexpr int L = B / E, BPW = 64 / L, NW = E / 8;  // NW words of nibbles per slice per lane
   static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4), "lane layout");
+  constexpr int YB = YDT < 0 ? 0 : E * elem_size<(YDT < 0 ? 0 : YDT)>();  // dequantised bytes per lane
+  constexpr bool YSTAGE = YB > 16;
+  __shared__ u32x4 ybuf[YSTAGE ? kThreads * YB / 16 : 1];
   const int lane = threadIdx.x & 63;
   const int64_t blk = wave_id() * BPW + lane / L;
   const bool valid = blk < nfull;
-  const int64_t byte0 = (blk * B + (int64_t)(lane % L) * E) >> 1;
+  const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
+  const int64_t byte0 = e0 >> 1;
   const uint8_t* src = in + byte0;
   const float* ssrc = sin + blk;
 
@@ -545,12 +556,29 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   uint32_t m[E];
 #pragma unroll
   for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
-  if (valid) {
+  if (out != nullptr && valid) {
     uint32_t o[NW];
 #pragma unroll
     for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
     store_words<ZQ_NT_REDUCE, NW>(out + byte0, o);
     if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
+  }
+  if constexpr (YDT >= 0) {
+    // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
+    float v[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
+    const int64_t wg_blk0 = (int64_t)blockIdx.x * (kThreads / 64) * BPW;
+    if (YSTAGE && wg_blk0 + (kThreads / 64) * BPW <= nfull) {  // workgroup-uniform
+      store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
+      __syncthreads();
+      u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + wg_blk0 * B * elem_size<YDT>());
+#pragma unroll
+      for (int c = 0; c < YB / 16; ++c)
+        st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
+    } else if (valid) {
+      store_elems<ZQ_NT_DEQ4, YDT, E>(y, e0, v);
+    }
   }
 }
 
@@ -561,7 +589,7 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
 __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                        int P, int64_t slice_bytes, int64_t slice_scales, int64_t m,
                                                        int B, int64_t blk_begin, uint8_t* __restrict__ out,
-                                                       float* __restrict__ sout) {
+                                                       float* __restrict__ sout, void* __restrict__ y, int ydt) {
   constexpr int MAXI = 1024 / 128;
   const int lane = threadIdx.x;
   const int64_t blk = blk_begin + blockIdx.x;
@@ -605,10 +633,22 @@ __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict
     if (j < nbytes) {
       const uint32_t lo = code_bits(acc[2 * i], r);
       const uint32_t hi = (2 * j + 1 < len) ? code_bits(acc[2 * i + 1], r) : 0u;
-      out[(base >> 1) + j] = (uint8_t)((lo & 0xfu) | ((hi & 0xfu) << 4));
+      if (out != nullptr) out[(base >> 1) + j] = (uint8_t)((lo & 0xfu) | ((hi & 0xfu) << 4));
+      if (y != nullptr) {
+        const float v0 = (u2f(lo) - kRoundMagic) * so, v1 = (u2f(hi) - kRoundMagic) * so;
+        const int64_t i0 = base + 2 * j;
+        if (ydt == ZQ_F32) store1<ZQ_F32>(y, i0, v0);
+        else if (ydt == ZQ_F16) store1<ZQ_F16>(y, i0, v0);
+        else store1<ZQ_BF16>(y, i0, v0);
+        if (2 * j + 1 < len) {
+          if (ydt == ZQ_F32) store1<ZQ_F32>(y, i0 + 1, v1);
+          else if (ydt == ZQ_F16) store1<ZQ_F16>(y, i0 + 1, v1);
+          else store1<ZQ_BF16>(y, i0 + 1, v1);
+        }
+      }
     }
   }
-  if (lane == 0) sout[blk] = so;
+  if (lane == 0 && out != nullptr) sout[blk] = so;
 }
 
 // ------------------------------------------------------------------ instantiation tables
@@ -658,15 +698,25 @@ DequantKernel dequant_kernel(int dt, int qbits) {
   return &k_dequant<ZQ_BF16, 4>;
 }
 
-ReduceKernel reduce_kernel(int lgB, bool small) {
+template <int YDT>
+static ReduceKernel reduce_kernel_for(int lgB, bool small) {
   constexpr int EL = kReduceElems, UL = ZQ_REDUCE_U, ES = kReduceElemsSmall, US = ZQ_REDUCE_U_SMALL;
   switch (lgB) {
-    case 5: return small ? &k_reduce<32, ES, US> : &k_reduce<32, EL, UL>;
-    case 6: return small ? &k_reduce<64, ES, US> : &k_reduce<64, EL, UL>;
-    case 7: return small ? &k_reduce<128, ES, US> : &k_reduce<128, EL, UL>;
-    case 8: return small ? &k_reduce<256, ES, US> : &k_reduce<256, EL, UL>;
-    case 9: return small ? &k_reduce<512, ES, US> : &k_reduce<512, EL, UL>;
-    default: return &k_reduce<1024, EL, UL>;  // a block may span at most one wave
+    case 5: return small ? &k_reduce<32, ES, US, YDT> : &k_reduce<32, EL, UL, YDT>;
+    case 6: return small ? &k_reduce<64, ES, US, YDT> : &k_reduce<64, EL, UL, YDT>;
+    case 7: return small ? &k_reduce<128, ES, US, YDT> : &k_reduce<128, EL, UL, YDT>;
+    case 8: return small ? &k_reduce<256, ES, US, YDT> : &k_reduce<256, EL, UL, YDT>;
+    case 9: return small ? &k_reduce<512, ES, US, YDT> : &k_reduce<512, EL, UL, YDT>;
+    default: return &k_reduce<1024, EL, UL, YDT>;  // a block may span at most one wave
+  }
+}
+
+ReduceKernel reduce_kernel(int lgB, bool small, int ydt) {
+  switch (ydt) {
+    case ZQ_F32: return reduce_kernel_for<ZQ_F32>(lgB, small);
+    case ZQ_F16: return reduce_kernel_for<ZQ_F16>(lgB, small);
+    case ZQ_BF16: return reduce_kernel_for<ZQ_BF16>(lgB, small);
+    default: return reduce_kernel_for<-1>(lgB, small);
   }
 }
 

@@ -32,7 +32,7 @@ def L():
 def test_header_declares_the_five_calls():
     names = _declared()
     for fn in ("qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-               "zq_num_scales", "zq_int4_bytes", "zq_status_string"):
+               "qgz_reduce_dequantize", "zq_num_scales", "zq_int4_bytes", "zq_status_string"):
         assert fn in names, fn
 
 
@@ -110,3 +110,22 @@ def test_reduce_argument_errors(L):
     assert f(vp(A), vp(C), 8, 256, 128, vp(A + 3 * 128), vp(B + 4096), None) == -8
     # output scales overlapping input scales
     assert f(vp(A), vp(C), 8, 256, 128, vp(B), vp(C + 8), None) == -8
+
+
+def test_reduce_dequantize_argument_errors(L):
+    f = L.qgz_reduce_dequantize
+    vp = ctypes.c_void_p
+    Y = 0x7F0030000000
+    assert f(vp(A), vp(C), 8, 256, 128, vp(Y), 5, None, None, None) == -3      # bad dtype
+    assert f(vp(A), vp(C), 8, 256, 128, vp(Y), -1, None, None, None) == -3     # bad dtype, no INT4 output
+    assert f(vp(A), vp(C), 0, 256, 128, vp(Y), 0, None, None, None) == -6
+    assert f(vp(A), vp(C), 8, 256, 96, vp(Y), 0, None, None, None) == -2
+    assert f(vp(A), vp(C), 8, -4, 128, vp(Y), 0, None, None, None) == -5
+    assert f(vp(A), vp(C), 8, 0, 128, None, 0, None, None, None) == 0
+    assert f(vp(A), vp(C), 8, 256, 128, None, 0, None, None, None) == -1       # y required
+    assert f(vp(A), vp(C), 8, 256, 128, vp(Y), 0, vp(B), None, None) == -1     # one INT4 pointer only
+    assert f(vp(A), vp(C), 8, 256, 128, vp(Y + 4), 0, None, None, None) == -4
+    assert f(vp(A), vp(C), 8, 256, 128, vp(A + 512), 0, None, None, None) == -8  # y over the slices
+    assert f(vp(A), vp(C), 8, 256, 128, vp(Y), 0, vp(Y + 512), vp(B), None) == -8  # y over packed_out
+    # the plain reduce still requires its INT4 outputs
+    assert L.qgz_reduce_level(vp(A), vp(C), 8, 256, 128, None, None, None) == -1

@@ -290,3 +290,29 @@ def test_argument_error_writes_nothing():
         zq.qgz_quantize(x, 48, packed=out, scales=sc)
     torch.cuda.synchronize()
     assert bool((out == 0x5A).all()) and bool((sc == 7.0).all())
+
+
+FUSED_CASES = [(2, 128, 524288, "f32"), (8, 128, (1 << 23) + 4096, "f32"), (48, 128, 4096 * 32, "f32"),
+               (3, 64, 65536 + 64, "bf16"), (4, 256, 8192, "f16"), (8, 128, 1000, "f32"), (2, 1024, 3072, "bf16"),
+               (5, 32, 33, "f32"), (2, 128, (1 << 22), "bf16"), (2, 128, (1 << 23) + 4096, "bf16")]
+
+
+@pytest.mark.parametrize("P,block,m,out", FUSED_CASES)
+def test_reduce_dequantize_fused(P, block, m, out):
+    """The fused last level equals dequantise(reduce_level(...)) bit for bit,
+    with and without the optional INT4 output."""
+    pin, sin = _slices(P, m, block, 97 * P + m + block)
+    po, so = oracle.qgz_reduce_level(pin, sin, P, m, block)
+    want = oracle.qgz_dequantize(po, so, m, block, out)
+    dt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[out]
+    dpin, dsin = to_dev(pin), to_dev(sin)
+    y = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(y), want, f"fused P={P} B={block} m={m} -> {out}")
+    gp = torch.empty(zq.int4_bytes(m), dtype=torch.uint8, device="cuda")
+    gs = torch.empty(zq.num_scales(m, block), dtype=torch.float32, device="cuda")
+    y2 = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt, packed_out=gp, scales_out=gs)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(y2), want, "fused (with INT4 output)")
+    assert_bits_equal(from_dev(gp), po, "fused INT4 packed")
+    assert_bits_equal(from_dev(gs), so, "fused INT4 scales")
