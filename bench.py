@@ -291,8 +291,8 @@ def load_traffic(call):
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
     ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
@@ -380,6 +380,24 @@ def main():
                         "fused_bytes": fused_bytes,
                         "fused_GBps": round(fused_bytes / (times["fused"] * 1e-6) / 1e9, 1)}
 
+    # next row: the degree-2 weight partition (1/2 shard quantised into its slot
+    # of the gathered buffer; the dequantisation of the gathered layer is the
+    # same call as in the step)
+    half = n // 2
+    sd2 = lambda: zq.qwz_quantize(L.w[:half], WBLOCK, codes=L.codes[:half], scales=L.wscales[:nsc(half, WBLOCK)])
+    for _ in range(3):
+        sd2()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        sd2()
+    e1.record()
+    torch.cuda.synchronize()
+    sd2_us = e0.elapsed_time(e1) * 1e3 / args.steps
+    sd2_bytes = bytes_qwz_quant(half, 2, WBLOCK)
+    sec_degree_2 = {"qwz_quantize half-shard us": round(sd2_us, 2), "bytes": sd2_bytes,
+                    "GBps": round(sd2_bytes / (sd2_us * 1e-6) / 1e9, 1)}
+
     # practical ceiling: a plain device-to-device copy of 1 GiB
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
@@ -408,6 +426,7 @@ def main():
                      "bytes_per_launch": dom_bytes, "us_per_launch": round(per_call_ms[dom] * 1e3, 2)},
         "kernels": kernels,
         "fused_last_level": fused,
+        "sec_degree_2": sec_degree_2,
         "copy_ceiling_GBps": round(copy_gbps, 1),
     }
 

@@ -7,7 +7,8 @@ inputs (the oracle is fast enough to compute whole tensors).
   1  1024x1024 fp16 weight, INT8 B=256 -> fp16; fp32 gradient, P=2, INT4 B=128
   2  GPT-1.3B-shaped layer (12 h^2, h=2048): bf16 weight shard 1/8 and full
      dequant; fp32 gradient, one level P=8
-  3  GPT-20B-shaped layer (h=6144): as 2 at 452,984,832 parameters
+  3  GPT-20B-shaped layer (h=6144): as 2 at 452,984,832 parameters; also the
+     degree-2 weight partition (1/2 shard, 2-shard gather)
   4  GPT-20B layer, three levels P = 2, 4, 48, final dequant to fp32
   5  123,456,789-element fp32 stress tensor (Student-t nu=3 x0.02, 0.1% x100
      outliers, zero groups), INT8 B=256 and INT4 B=64, dequant to bf16
@@ -114,6 +115,13 @@ def test_config2_gpt13b_layer():
 def test_config3_gpt20b_layer_weights():
     w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
     _qwz_case(3, w, "bf16", 256, 8, "bf16")
+
+
+def test_config3_sec_degree_2():
+    """The paper's degree-2 weight partition (primary over a GCD pair, Sec-Degree=2
+    secondary): a 1/2 shard quantised into its slot, the 2-shard gather dequantised."""
+    w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
+    _qwz_case(3, w, "bf16", 256, 2, "bf16")
 
 
 def test_config3_gpt20b_layer_gradients():
