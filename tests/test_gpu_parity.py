@@ -316,3 +316,64 @@ def test_reduce_dequantize_fused(P, block, m, out):
     assert_bits_equal(from_dev(y2), want, "fused (with INT4 output)")
     assert_bits_equal(from_dev(gp), po, "fused INT4 packed")
     assert_bits_equal(from_dev(gs), so, "fused INT4 scales")
+
+
+def test_repeat_runs_bit_identical():
+    """Every call is deterministic: two runs give identical bits."""
+    g = np.random.default_rng(21)
+    n, P, m = (1 << 21) + 1000, 8, 1 << 18
+    x = to_dev((g.standard_normal(n) * 1e-3).astype(np.float32))
+    pin, sin = _slices(P, m, 128, 5)
+    dpin, dsin = to_dev(pin), to_dev(sin)
+    outs = []
+    for _ in range(2):
+        c, s = zq.qwz_quantize(x, 256)
+        p4, s4 = zq.qgz_quantize(x, 128)
+        rp, rs = zq.qgz_reduce_level(dpin, dsin, P, m, 128)
+        y = zq.qgz_reduce_dequantize(dpin, dsin, P, m, 128)
+        d8 = zq.qwz_dequantize(c, s, 256, out_dtype=torch.bfloat16)
+        torch.cuda.synchronize()
+        outs.append([from_dev(t) for t in (c, s, p4, s4, rp, rs, y, d8)])
+    for a, b in zip(*outs):
+        assert a.tobytes() == b.tobytes()
+
+
+def test_hip_graph_capture_replays():
+    """The entry points enqueue only kernel launches (no allocation, memset or
+    synchronisation), so a sequence of calls can be captured in a HIP graph.
+    Each replay, with eager work in between, must give the eager bits."""
+    g = np.random.default_rng(22)
+    n, block = 1 << 20, 128
+    x_host = (g.standard_normal(n) * 1e-3).astype(np.float32)
+    x = to_dev(x_host)
+    P, m = 4, n // 4
+    packed = torch.empty(n // 2, dtype=torch.uint8, device="cuda")
+    scales = torch.empty(n // block, dtype=torch.float32, device="cuda")
+    rp = torch.empty(m // 2, dtype=torch.uint8, device="cuda")
+    rs = torch.empty(m // block, dtype=torch.float32, device="cuda")
+    y = torch.empty(m, dtype=torch.float32, device="cuda")
+    yf = torch.empty(m, dtype=torch.bfloat16, device="cuda")
+
+    def path():
+        zq.qgz_quantize(x, block, packed=packed, scales=scales)
+        zq.qgz_reduce_level(packed, scales, P, m, block, packed_out=rp, scales_out=rs)
+        zq.qgz_dequantize(rp, rs, m, block, y=y)
+        zq.qgz_reduce_dequantize(packed, scales, P, m, block, y=yf)
+
+    path()
+    torch.cuda.synchronize()
+    want = [from_dev(t).copy() for t in (packed, scales, rp, rs, y, yf)]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            path()
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in (packed, scales, rp, rs, y, yf):
+            t.zero_()                      # eager work between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        for t, w in zip((packed, scales, rp, rs, y, yf), want):
+            assert from_dev(t).tobytes() == w.tobytes(), f"replay {rep}"
