@@ -125,15 +125,17 @@ class Layer20B:
         T.cuda.synchronize()
         log(f"3-level chain ready ({time.time() - t0:.1f}s)")
 
-        # (name, bytes) of each launch, in step order
+        # (name, algorithmic bytes, elements) of each launch, in step order;
+        # elements = the elements of the tensor a call codes (P*m slice
+        # elements for a reduce level)
         self.calls = [
-            ("qwz_quantize", bytes_qwz_quant(self.shard, 2, WBLOCK)),
-            ("qwz_dequantize", bytes_qwz_deq(n, 2, WBLOCK)),
-            ("qgz_quantize", bytes_qgz_quant(n, 4, GBLOCK)),
-            ("qgz_reduce_level P=8", bytes_reduce(8, self.m8, GBLOCK)),
-            ("qgz_dequantize P=8 shard", bytes_qgz_deq(self.m8, 4, GBLOCK)),
-        ] + [(f"qgz_reduce_level P={P}", bytes_reduce(P, m, GBLOCK)) for P, m, _, _ in self.chain] + [
-            ("qgz_dequantize chain shard", bytes_qgz_deq(cur_m, 4, GBLOCK))]
+            ("qwz_quantize", bytes_qwz_quant(self.shard, 2, WBLOCK), self.shard),
+            ("qwz_dequantize", bytes_qwz_deq(n, 2, WBLOCK), n),
+            ("qgz_quantize", bytes_qgz_quant(n, 4, GBLOCK), n),
+            ("qgz_reduce_level P=8", bytes_reduce(8, self.m8, GBLOCK), 8 * self.m8),
+            ("qgz_dequantize P=8 shard", bytes_qgz_deq(self.m8, 4, GBLOCK), self.m8),
+        ] + [(f"qgz_reduce_level P={P}", bytes_reduce(P, m, GBLOCK), P * m) for P, m, _, _ in self.chain] + [
+            ("qgz_dequantize chain shard", bytes_qgz_deq(cur_m, 4, GBLOCK), cur_m)]
 
     def _level_buffers(self, P, m, own_p, own_s, key):
         """All-to-all receive buffer of one level at local rank 0: slice 0 is
@@ -341,14 +343,15 @@ def main():
 
     per_call_ms = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(ncalls)]
                             for k in range(args.steps)]).mean(axis=0)
-    step_bytes = sum(b for _, b in L.calls)
+    step_bytes = sum(b for _, b, _ in L.calls)
+    step_elems = sum(e for _, _, e in L.calls)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = []
-    for (name, b), ms in zip(L.calls, per_call_ms):
-        kernels.append({"call": name, "bytes": b, "us": round(ms * 1e3, 2),
-                        "GBps": round(b / (ms * 1e-3) / 1e9, 1)})
+    for (name, b, e), ms in zip(L.calls, per_call_ms):
+        kernels.append({"call": name, "bytes": b, "elements": e, "us": round(ms * 1e3, 2),
+                        "GBps": round(b / (ms * 1e-3) / 1e9, 1), "Gelem_per_s": round(e / (ms * 1e-3) / 1e9, 1)})
     dom = max(range(ncalls), key=lambda i: per_call_ms[i])
-    dom_name, dom_bytes = L.calls[dom]
+    dom_name, dom_bytes, _ = L.calls[dom]
     achieved = dom_bytes / (per_call_ms[dom] * 1e-3) / 1e9
     traffic = load_traffic(dom_name)
 
@@ -419,8 +422,9 @@ def main():
         "config": {"workload": "gpt-20b-layer qwZ/qgZ step (h=6144, ffn=24576, n=452,984,832): "
                                "qwz shard 1/8 bf16 B=256 + gathered dequant -> bf16; qgz fp32 B=128, "
                                "P=8 level + 3-level chain P=2/4/48, final dequant -> fp32",
-                   "n": n, "step_bytes": step_bytes, "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 1),
-                   "elements_per_s": round(sum(nn for nn in (L.shard, n, n, L.m8 * 8, L.m8)) / (ms_per_step * 1e-3))},
+                   "n": n, "step_bytes": step_bytes, "step_elements": step_elems,
+                   "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 1),
+                   "elements_per_s": round(step_elems / (ms_per_step * 1e-3))},
         "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "us_per_launch": round(per_call_ms[dom] * 1e3, 2)},

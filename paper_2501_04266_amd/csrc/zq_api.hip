@@ -91,7 +91,7 @@ int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, floa
 
   const int64_t nfull = n / block;
   const int64_t blocks_per_wave = 64 / (block / quant_elems((int)elem_bytes(xt), block));
-  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64);
+  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64 * kQuantTiles);
   if (grid == 0) return ZQ_E_SIZE;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -168,14 +168,16 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
   const bool vector_path = m % 32 == 0;
   const int64_t nfull = vector_path ? m / block : 0;
   const int64_t waves_large = (nfull + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
-  const bool small = block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES;
-  const int64_t blocks_per_wave = 64 / (block / (small ? kReduceElemsSmall : kReduceElems));
-  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64);
+  ReduceShape shape = ReduceShape::kLarge;
+  if (block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES) shape = ReduceShape::kSmall;
+  else if (block <= 512 && P <= 2 && !fused) shape = ReduceShape::kTwoSlices;
+  const int64_t blocks_per_wave = 64 / (block / reduce_elems(shape));
+  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64 * reduce_tiles(shape));
   if (grid == 0) return ZQ_E_SIZE;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (nfull > 0) {
-    int rc = launch(reduce_kernel(lgB, small, fused ? yt : -1), (unsigned)grid, kThreads, st, packed_in, scales_in,
+    int rc = launch(reduce_kernel(lgB, shape, fused ? yt : -1), (unsigned)grid, kThreads, st, packed_in, scales_in,
                     (int)P, slice_bytes, nb, nfull, packed_out, scales_out, y);
     if (rc != ZQ_OK) return rc;
   }

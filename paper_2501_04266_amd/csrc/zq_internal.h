@@ -10,6 +10,10 @@ constexpr int kThreads = 256;  // threads per workgroup of the streaming kernels
 #define ZQ_QUANT_THREADS 256
 #endif
 constexpr int kQuantThreads = ZQ_QUANT_THREADS;
+#ifndef ZQ_QUANT_TILES
+#define ZQ_QUANT_TILES 1
+#endif
+constexpr int kQuantTiles = ZQ_QUANT_TILES;  // wave tiles per wave in the quantiser
 #ifndef ZQ_DEQ_THREADS
 #define ZQ_DEQ_THREADS 256
 #endif
@@ -50,6 +54,12 @@ constexpr int deq4_elems(int out_bytes) { return out_bytes == 4 ? ZQ_DEQ4_E_F32 
 #endif
 constexpr int kReduceElems = ZQ_REDUCE_E;  // 16 bytes of every slice per lane
 constexpr int kReduceElemsSmall = 8;  // 4 bytes per slice per lane, for small levels
+// Launch shapes of the reduce level (see the kernel): 32 elements per lane
+// and 4 slices ahead; the same for P <= 2 with two tiles per wave; 8 elements
+// per lane and 16 slices ahead for levels with few waves.
+enum class ReduceShape { kLarge, kTwoSlices, kSmall };
+constexpr int reduce_elems(ReduceShape s) { return s == ReduceShape::kSmall ? 8 : 32; }
+constexpr int reduce_tiles(ReduceShape s) { return s == ReduceShape::kTwoSlices ? 2 : 1; }
 // A level whose E = 32 launch would have fewer waves than this runs the small
 // variant (4x the waves, more slices in flight per wave).
 #ifndef ZQ_REDUCE_SMALL_WAVES
@@ -67,7 +77,7 @@ QuantKernel quant_kernel(int dt, int qbits, int lgB);
 QuantTailKernel quant_tail_kernel(int dt, int qbits);
 DequantKernel dequant_kernel(int dt, int qbits);
 // ydt < 0: INT4 output only; otherwise also the fused dequantisation to ydt
-ReduceKernel reduce_kernel(int lgB, bool small, int ydt);
+ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
 ReduceGenericKernel reduce_generic_kernel();
 
 }  // namespace zq

@@ -291,74 +291,86 @@ template <int DT, int QBITS, int B>
 __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restrict__ x, int64_t nfull,
                                                             uint8_t* __restrict__ out, float* __restrict__ scales) {
   constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
+  constexpr int T = kQuantTiles, WAVES = kQuantThreads / 64;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
-  constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane
-  constexpr int WG_BLOCKS = kQuantThreads / 64 * BPW;           // blocks per workgroup
-  constexpr int WG_BYTES = kQuantThreads * OB;                  // code bytes per workgroup
+  constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane and tile
+  constexpr int WG_BLOCKS = WAVES * T * BPW;                    // blocks per workgroup
+  constexpr int WG_BYTES = WAVES * T * 64 * OB;                 // code bytes per workgroup
+  constexpr int NWO = OB >= 4 ? OB / 4 : 1;
   static_assert(E % 4 == 0 && L >= 1 && L <= 64 && WG_BYTES % 16 == 0, "lane layout");
   __shared__ u32x4 obuf[WG_BYTES / 16];
   __shared__ float sbuf[WG_BLOCKS];
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int64_t blk = wave_id() * BPW + lane / L;
-  const bool valid = blk < nfull;
-  const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
-  float v[E];
-  if (valid) {
-    load_elems<ZQ_NT_QUANT, DT, E>(x, e0, v);
-  } else {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // workgroup g owns tiles [g*WAVES*T, (g+1)*WAVES*T); its t-th round of loads
+  // covers WAVES adjacent tiles, one per wave
+  const int64_t wg_blk0 = (int64_t)blockIdx.x * WG_BLOCKS;
+  float v[T][E];
 #pragma unroll
-    for (int k = 0; k < E; ++k) v[k] = 0.0f;
-  }
-  float a = fabsf(v[0]);
-#pragma unroll
-  for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(v[k]));
-  const float amax = u2f(group_max<L>(f2u(a)));
-  float s = 0.0f, r = 0.0f;
-  if (amax >= kFlushBelow) {
-    s = scale_of<(int)QMAX>(amax);
-    r = QMAX / amax;
-  }
-  uint32_t m[E];
-#pragma unroll
-  for (int k = 0; k < E; ++k) m[k] = code_bits(v[k], r);
-
-  // this lane's packed codes: OB bytes, little-endian in w
-  constexpr int NWO = OB >= 4 ? OB / 4 : 1;
-  uint32_t w[NWO];
-  if constexpr (QBITS == 8) {
-#pragma unroll
-    for (int k = 0; k < E / 4; ++k) w[k] = pack_bytes4(m[4 * k], m[4 * k + 1], m[4 * k + 2], m[4 * k + 3]);
-  } else if constexpr (E == 4) {
-    w[0] = (m[0] & 0xfu) | ((m[1] & 0xfu) << 4) | ((m[2] & 0xfu) << 8) | ((m[3] & 0xfu) << 12);
-  } else {
-#pragma unroll
-    for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
-  }
-
-  const int64_t wg_blk0 = (blk - lane / L) - (int64_t)(tid >> 6) * BPW;  // first block of the workgroup
-  if (wg_blk0 + WG_BLOCKS <= nfull) {  // workgroup-uniform
-    char* ob = reinterpret_cast<char*>(obuf) + tid * OB;
-    if constexpr (OB == 2) {
-      *reinterpret_cast<uint16_t*>(ob) = (uint16_t)w[0];
+  for (int t = 0; t < T; ++t) {
+    const int64_t blk = wg_blk0 + (t * WAVES + wave) * BPW + lane / L;
+    if (blk < nfull) {
+      load_elems<ZQ_NT_QUANT, DT, E>(x, blk * B + (int64_t)(lane % L) * E, v[t]);
     } else {
 #pragma unroll
-      for (int k = 0; k < NWO; ++k) reinterpret_cast<uint32_t*>(ob)[k] = w[k];
+      for (int k = 0; k < E; ++k) v[t][k] = 0.0f;
     }
-    if (lane % L == 0) sbuf[(tid >> 6) * BPW + lane / L] = s;
+  }
+  const bool full = wg_blk0 + WG_BLOCKS <= nfull;  // workgroup-uniform
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    const int slot = t * WAVES + wave;              // tile index within the workgroup
+    const int64_t blk = wg_blk0 + slot * BPW + lane / L;
+    float a = fabsf(v[t][0]);
+#pragma unroll
+    for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(v[t][k]));
+    const float amax = u2f(group_max<L>(f2u(a)));
+    float s = 0.0f, r = 0.0f;
+    if (amax >= kFlushBelow) {
+      s = scale_of<(int)QMAX>(amax);
+      r = QMAX / amax;
+    }
+    uint32_t m[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) m[k] = code_bits(v[t][k], r);
+
+    // this lane's packed codes: OB bytes, little-endian in w
+    uint32_t w[NWO];
+    if constexpr (QBITS == 8) {
+#pragma unroll
+      for (int k = 0; k < E / 4; ++k) w[k] = pack_bytes4(m[4 * k], m[4 * k + 1], m[4 * k + 2], m[4 * k + 3]);
+    } else if constexpr (E == 4) {
+      w[0] = (m[0] & 0xfu) | ((m[1] & 0xfu) << 4) | ((m[2] & 0xfu) << 8) | ((m[3] & 0xfu) << 12);
+    } else {
+#pragma unroll
+      for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
+    }
+
+    if (full) {
+      char* ob = reinterpret_cast<char*>(obuf) + (slot * 64 + lane) * OB;
+      if constexpr (OB == 2) {
+        *reinterpret_cast<uint16_t*>(ob) = (uint16_t)w[0];
+      } else {
+#pragma unroll
+        for (int k = 0; k < NWO; ++k) reinterpret_cast<uint32_t*>(ob)[k] = w[k];
+      }
+      if (lane % L == 0) sbuf[slot * BPW + lane / L] = s;
+    } else if (blk < nfull) {
+      uint8_t* dst = out + ((blk * B + (int64_t)(lane % L) * E) * OB) / E;
+      if constexpr (OB == 2) {
+        st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(dst), (uint16_t)w[0]);
+      } else {
+        store_words<ZQ_NT_QUANT, NWO>(dst, w);
+      }
+      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
+    }
+  }
+  if (full) {
     __syncthreads();
     u32x4* dst = reinterpret_cast<u32x4*>(out + (wg_blk0 * B * OB) / E);
 #pragma unroll
     for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<ZQ_NT_QUANT>(dst + c, obuf[c]);
     if (tid < WG_BLOCKS) st<2 * ZQ_NT_SCALES>(scales + wg_blk0 + tid, sbuf[tid]);
-  } else if (valid) {
-    uint8_t* dst = out + (e0 * OB) / E;
-    if constexpr (OB == 2) {
-      st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(dst), (uint16_t)w[0]);
-    } else {
-      store_words<ZQ_NT_QUANT, NWO>(dst, w);
-    }
-    if (lane % L == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
   }
 }
 
@@ -472,28 +484,42 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
 // bytes per lane are staged in LDS and written as wave-contiguous 16-byte
 // stores, as in the dequantiser.
 
-template <int B, int E, int U, int YDT>
+template <int B, int E, int U, int TR, int YDT>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
                                                      float* __restrict__ sout, void* __restrict__ y) {
   constexpr int L = B / E, BPW = 64 / L, NW = E / 8;  // NW words of nibbles per slice per lane
-  static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4), "lane layout");
+  static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4) && TR >= 1, "lane layout");
   constexpr int YB = YDT < 0 ? 0 : E * elem_size<(YDT < 0 ? 0 : YDT)>();  // dequantised bytes per lane
-  constexpr bool YSTAGE = YB > 16;
+  constexpr bool YSTAGE = YB > 16 && TR == 1;
   __shared__ u32x4 ybuf[YSTAGE ? kThreads * YB / 16 : 1];
   const int lane = threadIdx.x & 63;
-  const int64_t blk = wave_id() * BPW + lane / L;
-  const bool valid = blk < nfull;
-  const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
-  const int64_t byte0 = e0 >> 1;
-  const uint8_t* src = in + byte0;
-  const float* ssrc = sin + blk;
+
+  uint32_t w[U][NW];
+  float s[U];
+  // loads of slices [p0, p0 + U) of the tile starting at block blk (lane's block)
+  auto load_batch = [&](int64_t blk, int p0) {
+    const bool valid = blk < nfull;
+    const int64_t byte0 = (blk * B + (int64_t)(lane % L) * E) >> 1;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = p0 + u;
+      if (valid && p < P) {
+        load_words<ZQ_NT_REDUCE, NW>(in + byte0 + (int64_t)p * slice_bytes, w[u]);
+        s[u] = ld<ZQ_NT_REDUCE>(sin + blk + (int64_t)p * slice_scales);
+      } else {
+#pragma unroll
+        for (int j = 0; j < NW; ++j) w[u][j] = 0u;
+        s[u] = 0.0f;
+      }
+    }
+  };
 
   float acc[E];
   // one slice into the sum, word by word (8 products live at a time)
-  auto accumulate = [&](const uint32_t (&ww)[NW], float s, bool first) {
-    const float s16 = s * 16.0f;
+  auto accumulate = [&](const uint32_t (&ww)[NW], float sc, bool first) {
+    const float s16 = sc * 16.0f;
     if (__all(s16 <= kMaxFloat)) {  // wave-uniform: 16*s exact for every lane
 #pragma unroll
       for (int j = 0; j < NW; ++j) {
@@ -512,72 +538,70 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
         nibbles_over_16(ww[j], f);
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
-          const float prod = (f[k] * 16.0f) * s;
+          const float prod = (f[k] * 16.0f) * sc;
           acc[8 * j + k] = first ? prod : acc[8 * j + k] + prod;
         }
       }
     }
   };
 
-  for (int p0 = 0; p0 < P; p0 += U) {
-    uint32_t w[U][NW];
-    float s[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int p = p0 + u;
-      if (valid && p < P) {
-        load_words<ZQ_NT_REDUCE, NW>(src + (int64_t)p * slice_bytes, w[u]);
-        s[u] = ld<ZQ_NT_REDUCE>(ssrc + (int64_t)p * slice_scales);
+  const int64_t wave0 = wave_id() * TR;
+  load_batch(wave0 * BPW + lane / L, 0);
+#pragma unroll 1
+  for (int t = 0; t < TR; ++t) {
+    const int64_t blk = (wave0 + t) * BPW + lane / L;
+    const bool valid = blk < nfull;
+    const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
+    const int64_t byte0 = e0 >> 1;
+    for (int p0 = 0; p0 < P; p0 += U) {
+      if (p0 > 0) load_batch(blk, p0);
+      if (p0 == 0) {
+        accumulate(w[0], s[0], true);
       } else {
-#pragma unroll
-        for (int j = 0; j < NW; ++j) w[u][j] = 0u;
-        s[u] = 0.0f;
+        accumulate(w[0], s[0], false);
       }
-    }
-    if (p0 == 0) {
-      accumulate(w[0], s[0], true);
-    } else {
-      accumulate(w[0], s[0], false);
-    }
 #pragma unroll
-    for (int u = 1; u < U; ++u)
-      if (p0 + u < P) accumulate(w[u], s[u], false);
-  }
+      for (int u = 1; u < U; ++u)
+        if (p0 + u < P) accumulate(w[u], s[u], false);
+    }
+    // next tile's first batch goes out before this tile's requantisation
+    if (t + 1 < TR) load_batch(blk + BPW, 0);
 
-  float a = fabsf(acc[0]);
+    float a = fabsf(acc[0]);
 #pragma unroll
-  for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
-  const float amax = u2f(group_max<L>(f2u(a)));
-  float so = 0.0f, r = 0.0f;
-  if (amax >= kFlushBelow) {
-    so = scale_of<7>(amax);
-    r = 7.0f / amax;
-  }
-  uint32_t m[E];
+    for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
+    const float amax = u2f(group_max<L>(f2u(a)));
+    float so = 0.0f, r = 0.0f;
+    if (amax >= kFlushBelow) {
+      so = scale_of<7>(amax);
+      r = 7.0f / amax;
+    }
+    uint32_t m[E];
 #pragma unroll
-  for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
-  if (out != nullptr && valid) {
-    uint32_t o[NW];
+    for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
+    if (out != nullptr && valid) {
+      uint32_t o[NW];
 #pragma unroll
-    for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
-    store_words<ZQ_NT_REDUCE, NW>(out + byte0, o);
-    if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
-  }
-  if constexpr (YDT >= 0) {
-    // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
-    float v[E];
+      for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
+      store_words<ZQ_NT_REDUCE, NW>(out + byte0, o);
+      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
+    }
+    if constexpr (YDT >= 0) {
+      // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
+      float v[E];
 #pragma unroll
-    for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
-    const int64_t wg_blk0 = (int64_t)blockIdx.x * (kThreads / 64) * BPW;
-    if (YSTAGE && wg_blk0 + (kThreads / 64) * BPW <= nfull) {  // workgroup-uniform
-      store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
-      __syncthreads();
-      u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + wg_blk0 * B * elem_size<YDT>());
+      for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
+      const int64_t wg_blk0 = (int64_t)blockIdx.x * (kThreads / 64) * BPW;
+      if (YSTAGE && wg_blk0 + (kThreads / 64) * BPW <= nfull) {  // workgroup-uniform
+        store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
+        __syncthreads();
+        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + wg_blk0 * B * elem_size<YDT>());
 #pragma unroll
-      for (int c = 0; c < YB / 16; ++c)
-        st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
-    } else if (valid) {
-      store_elems<ZQ_NT_DEQ4, YDT, E>(y, e0, v);
+        for (int c = 0; c < YB / 16; ++c)
+          st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
+      } else if (valid) {
+        store_elems<ZQ_NT_DEQ4, YDT, E>(y, e0, v);
+      }
     }
   }
 }
@@ -699,24 +723,33 @@ DequantKernel dequant_kernel(int dt, int qbits) {
 }
 
 template <int YDT>
-static ReduceKernel reduce_kernel_for(int lgB, bool small) {
+static ReduceKernel reduce_kernel_for(int lgB, ReduceShape shape) {
+  // large: E = 32, U = 4; two slices: E = 32, U = 2, two tiles per wave with the
+  // next tile's loads issued before this tile's requantisation; small: E = 8,
+  // U = 16.  A block may span at most one wave, so B = 1024 always takes large.
   constexpr int EL = kReduceElems, UL = ZQ_REDUCE_U, ES = kReduceElemsSmall, US = ZQ_REDUCE_U_SMALL;
+#define ZQ_REDUCE_CASE(LG, BB)                                                                       \
+  case LG:                                                                                           \
+    if (shape == ReduceShape::kSmall) return &k_reduce<BB, ES, US, 1, YDT>;                          \
+    if (shape == ReduceShape::kTwoSlices) return &k_reduce<BB, EL, 2, 2, YDT>;                       \
+    return &k_reduce<BB, EL, UL, 1, YDT>;
   switch (lgB) {
-    case 5: return small ? &k_reduce<32, ES, US, YDT> : &k_reduce<32, EL, UL, YDT>;
-    case 6: return small ? &k_reduce<64, ES, US, YDT> : &k_reduce<64, EL, UL, YDT>;
-    case 7: return small ? &k_reduce<128, ES, US, YDT> : &k_reduce<128, EL, UL, YDT>;
-    case 8: return small ? &k_reduce<256, ES, US, YDT> : &k_reduce<256, EL, UL, YDT>;
-    case 9: return small ? &k_reduce<512, ES, US, YDT> : &k_reduce<512, EL, UL, YDT>;
-    default: return &k_reduce<1024, EL, UL, YDT>;  // a block may span at most one wave
+    ZQ_REDUCE_CASE(5, 32)
+    ZQ_REDUCE_CASE(6, 64)
+    ZQ_REDUCE_CASE(7, 128)
+    ZQ_REDUCE_CASE(8, 256)
+    ZQ_REDUCE_CASE(9, 512)
+    default: return &k_reduce<1024, EL, UL, 1, YDT>;
   }
+#undef ZQ_REDUCE_CASE
 }
 
-ReduceKernel reduce_kernel(int lgB, bool small, int ydt) {
+ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt) {
   switch (ydt) {
-    case ZQ_F32: return reduce_kernel_for<ZQ_F32>(lgB, small);
-    case ZQ_F16: return reduce_kernel_for<ZQ_F16>(lgB, small);
-    case ZQ_BF16: return reduce_kernel_for<ZQ_BF16>(lgB, small);
-    default: return reduce_kernel_for<-1>(lgB, small);
+    case ZQ_F32: return reduce_kernel_for<ZQ_F32>(lgB, shape);
+    case ZQ_F16: return reduce_kernel_for<ZQ_F16>(lgB, shape);
+    case ZQ_BF16: return reduce_kernel_for<ZQ_BF16>(lgB, shape);
+    default: return reduce_kernel_for<-1>(lgB, shape);
   }
 }
 

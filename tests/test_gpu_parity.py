@@ -183,7 +183,8 @@ for P in (1, 2, 3, 4, 8, 48):
         for m in (32, 2048 * 3 + block, 65536 + 128):
             REDUCE_CASES.append((P, block, m))
 # levels large enough for the 32-elements-per-lane variant (>= 4096 waves)
-for P, block, m in ((3, 128, (1 << 23) + 4096), (2, 64, (1 << 23) + 2048), (2, 256, (1 << 24) + 256)):
+for P, block, m in ((3, 128, (1 << 23) + 4096), (2, 64, (1 << 23) + 2048), (2, 256, (1 << 24) + 256),
+                    (1, 128, (1 << 23) + 4096), (2, 32, (1 << 22) + 1024)):
     REDUCE_CASES.append((P, block, m))
 # ragged m: not a multiple of the block, of 32, odd
 for P, block, m in ((2, 128, 1000), (3, 64, 999), (8, 128, 65536 + 77), (48, 64, 4095), (5, 1024, 3000),
