@@ -19,6 +19,13 @@ all-to-all of each level) are outside this path: their results are placed
 in HBM before timing (peer slices are quantised from seeded fp32 peer
 gradients; a level's local slice is chunk 0 of the previous level's output).
 
+Timing: W warm-up steps; a breakdown pass of K steps with HIP events between
+all calls (per-call figures, the `kernels` list); then the timed region of K
+steps, host wall clock between two device synchronisations, with one event
+pair around the dominant kernel only (its per-launch duration gives the
+roofline figure).  Events between launches cost GPU time, so the step time
+is never taken from the breakdown pass.
+
 Output: one JSON line.  value = algorithmic bytes of the step / step time.
 """
 import argparse
@@ -35,6 +42,7 @@ METRIC = "achieved HBM GB/s (% of MI355X peak) for qwZ quant/dequant + qgZ reduc
 HBM_PEAK_GBPS = 8000.0
 WBLOCK, GBLOCK, SHARD = 256, 128, 8
 FANINS = [2, 4, 48]
+COPY_REPS = 20
 
 
 def nsc(n, b):
@@ -157,13 +165,22 @@ class Layer20B:
         self.host[("peers",) + tuple(key)] = peers
         return pin, sin
 
-    def step(self, ev=None):
+    def step(self, ev=None, around=None):
+        """One pass of the path.  ev: events recorded before the first call,
+        between calls and after the last (len(calls) + 1 of them); with
+        `around` = i, only the pair ev[0], ev[1] around call i."""
         zq = self.zq
         n, s = self.n, self.shard
 
         def mark(i):
-            if ev is not None:
+            if ev is None:
+                return
+            if around is None:
                 ev[i].record()
+            elif i == around:
+                ev[0].record()
+            elif i == around + 1:
+                ev[1].record()
 
         mark(0)
         zq.qwz_quantize(self.w[:s], WBLOCK, codes=self.codes[:s], scales=self.wscales[:nsc(s, WBLOCK)])
@@ -265,6 +282,7 @@ def check_against_oracle(L, outs):
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2501_04266_amd", "csrc", f)
                   for f in ("zq_kernels.hip", "zq_internal.h", "zq_api.hip")]
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_pmc_traffic.txt")
+VALU_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_pmc_valu.txt")
 
 
 def kernel_source_hash():
@@ -290,6 +308,34 @@ def load_traffic(call):
     return None
 
 
+def load_valu(call):
+    """VALU figures per launch of `call` from the committed rocprofv3 PMC summary
+    (SQ_INSTS_VALU, GRBM_GUI_ACTIVE), or None when there is none for the call or
+    it was taken on different kernel sources."""
+    if not os.path.exists(VALU_PROFILE):
+        return None
+    lines = open(VALU_PROFILE).read().splitlines()
+    tag = "# kernel source sha256[:16]:"
+    h = next((ln[len(tag):].strip() for ln in lines if ln.startswith(tag)), None)
+    if h != kernel_source_hash():
+        return None
+    for ln in lines:
+        if ln.startswith(call + " ") and not ln.startswith("#"):
+            rest = ln[len(call):].split()
+            return {"valu_insts_per_elem": float(rest[1]), "valu_busy": float(rest[3])}
+    return None
+
+
+def cpu_model():
+    try:
+        for ln in open("/proc/cpuinfo"):
+            if ln.startswith("model name"):
+                return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -298,6 +344,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
     ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
+    ap.add_argument("--no-single-thread", action="store_true", help="skip the 1-thread oracle step")
     ap.add_argument("--n", type=int, default=0, help=argparse.SUPPRESS)  # smaller layer for quick checks
     args = ap.parse_args()
 
@@ -331,28 +378,44 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup {args.warmup} done")
 
+    # breakdown pass (not the timed region): HIP events between all calls of
+    # each step; an event between two launches costs about 3 us of GPU time,
+    # so these figures are per call but the step time is not taken here
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ncalls + 1)] for _ in range(args.steps)]
+    for k in range(args.steps):
+        L.step(evs[k])
+    torch.cuda.synchronize()
+    call_ms = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(ncalls)]
+                        for k in range(args.steps)])
+    per_call_ms, per_call_med = call_ms.mean(axis=0), np.median(call_ms, axis=0)
+    dom = max(range(ncalls), key=lambda i: per_call_ms[i])
+    dom_name, dom_bytes, _ = L.calls[dom]
+
+    # timed region: K steps; the only events recorded are the pair around the
+    # dominant kernel, which gives the roofline figure
+    dev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for k in range(args.steps):
-        L.step(evs[k])
+        L.step(dev[k], around=dom)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    dom_ms = np.array([dev[k][0].elapsed_time(dev[k][1]) for k in range(args.steps)])
 
-    per_call_ms = np.array([[evs[k][i].elapsed_time(evs[k][i + 1]) for i in range(ncalls)]
-                            for k in range(args.steps)]).mean(axis=0)
     step_bytes = sum(b for _, b, _ in L.calls)
     step_elems = sum(e for _, _, e in L.calls)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
     kernels = []
-    for (name, b, e), ms in zip(L.calls, per_call_ms):
-        kernels.append({"call": name, "bytes": b, "elements": e, "us": round(ms * 1e3, 2),
-                        "GBps": round(b / (ms * 1e-3) / 1e9, 1), "Gelem_per_s": round(e / (ms * 1e-3) / 1e9, 1)})
-    dom = max(range(ncalls), key=lambda i: per_call_ms[i])
-    dom_name, dom_bytes, _ = L.calls[dom]
-    achieved = dom_bytes / (per_call_ms[dom] * 1e-3) / 1e9
+    for (name, b, e), ms, med in zip(L.calls, per_call_ms, per_call_med):
+        k = {"call": name, "bytes": b, "elements": e, "us": round(ms * 1e3, 2), "us_median": round(med * 1e3, 2),
+             "GBps": round(b / (ms * 1e-3) / 1e9, 1), "Gelem_per_s": round(e / (ms * 1e-3) / 1e9, 1)}
+        valu = load_valu(name)
+        if valu is not None:
+            k["valu"] = valu
+        kernels.append(k)
+    achieved = dom_bytes / (dom_ms.mean() * 1e-3) / 1e9
     traffic = load_traffic(dom_name)
 
     # next row: the last level fused with the final dequantisation, against the
@@ -404,14 +467,15 @@ def main():
     # practical ceiling: a plain device-to-device copy of 1 GiB
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
-    dst.copy_(src)
+    for _ in range(3):
+        dst.copy_(src)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(5):
+    for _ in range(COPY_REPS):
         dst.copy_(src)
     e1.record()
     torch.cuda.synchronize()
-    copy_gbps = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    copy_gbps = COPY_REPS * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
     del src, dst
 
     out = {
@@ -427,7 +491,8 @@ def main():
                    "elements_per_s": round(step_elems / (ms_per_step * 1e-3))},
         "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "bytes_per_launch": dom_bytes, "us_per_launch": round(per_call_ms[dom] * 1e3, 2)},
+                     "bytes_per_launch": dom_bytes, "us_per_launch": round(dom_ms.mean() * 1e3, 2),
+                     "us_median": round(float(np.median(dom_ms)) * 1e3, 2)},
         "kernels": kernels,
         "fused_last_level": fused,
         "sec_degree_2": sec_degree_2,
@@ -440,9 +505,14 @@ def main():
         secs, outs = oracle_step(L, threads, args.cpu_repeats)
         bad = check_against_oracle(L, outs)
         out["cpu_baseline"] = {"value": round(step_bytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
-                               "kind": "oracle", "seconds_per_step": round(secs, 3),
+                               "kind": "oracle", "seconds_per_step": round(secs, 3), "cpu_model": cpu_model(),
                                "sample": f"the full step of the same workload (all calls, full sizes), each timed "
                                          f"call repeated {args.cpu_repeats}x, mean"}
+        if threads > 1 and not args.no_single_thread:
+            log("oracle step on 1 thread ...")
+            secs1, _ = oracle_step(L, 1, 1)
+            out["cpu_baseline"]["single_thread"] = {"value": round(step_bytes / secs1 / 1e9, 3),
+                                                    "seconds_per_step": round(secs1, 3)}
         out["parity"] = "bit-exact vs oracle (all step outputs)" if not bad else f"MISMATCH: {bad}"
         log(f"oracle {secs:.1f}s; parity: {out['parity']}")
     print(json.dumps(out), flush=True)

@@ -163,26 +163,29 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
       if (overlap(outs[o], outs[o2])) return ZQ_E_ALIAS;
   }
 
-  // every slice starts 16-byte aligned when m % 32 == 0: vector path over the
-  // full blocks, 64 lanes x E elements per wave
+  // every slice starts 16-byte aligned when m % 32 == 0: vector path over
+  // whole groups of blocks (4 wave tiles of 64 lanes x E elements each)
   const bool vector_path = m % 32 == 0;
-  const int64_t nfull = vector_path ? m / block : 0;
-  const int64_t waves_large = (nfull + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
+  const int64_t full_blocks = vector_path ? m / block : 0;
+  const int64_t waves_large = (full_blocks + 64 / (block / kReduceElems) - 1) / (64 / (block / kReduceElems));
   ReduceShape shape = ReduceShape::kLarge;
   if (block <= 512 && waves_large < ZQ_REDUCE_SMALL_WAVES) shape = ReduceShape::kSmall;
   else if (block <= 512 && P <= 2 && !fused) shape = ReduceShape::kTwoSlices;
-  const int64_t blocks_per_wave = 64 / (block / reduce_elems(shape));
-  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kThreads / 64 * reduce_tiles(shape));
-  if (grid == 0) return ZQ_E_SIZE;
+  const int64_t group_blocks = kThreads / 64 * (64 / (block / reduce_elems(shape)));
+  const int64_t groups = full_blocks / group_blocks;
+  const int64_t nfull = groups * group_blocks;
+  const int64_t grid = grid_for(groups, reduce_tiles(shape));
+  if (grid == 0 && groups > 0) return ZQ_E_SIZE;
 
   hipStream_t st = static_cast<hipStream_t>(stream);
-  if (nfull > 0) {
+  if (groups > 0) {
     int rc = launch(reduce_kernel(lgB, shape, fused ? yt : -1), (unsigned)grid, kThreads, st, packed_in, scales_in,
                     (int)P, slice_bytes, nb, nfull, packed_out, scales_out, y);
     if (rc != ZQ_OK) return rc;
   }
-  // remaining blocks (a short last block, or all of them when slices are not
-  // 16-byte aligned): one wave per block
+  // remaining blocks (those after the last whole group, including a short
+  // last block, or all of them when slices are not 16-byte aligned): one wave
+  // per block
   for (int64_t b0 = nfull; b0 < nb; b0 += (1LL << 30)) {
     const int64_t cnt = (nb - b0) < (1LL << 30) ? (nb - b0) : (1LL << 30);
     int rc = launch(reduce_generic_kernel(), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes, nb, m,

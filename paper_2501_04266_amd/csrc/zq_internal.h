@@ -55,11 +55,23 @@ constexpr int deq4_elems(int out_bytes) { return out_bytes == 4 ? ZQ_DEQ4_E_F32 
 constexpr int kReduceElems = ZQ_REDUCE_E;  // 16 bytes of every slice per lane
 constexpr int kReduceElemsSmall = 8;  // 4 bytes per slice per lane, for small levels
 // Launch shapes of the reduce level (see the kernel): 32 elements per lane
-// and 4 slices ahead; the same for P <= 2 with two tiles per wave; 8 elements
-// per lane and 16 slices ahead for levels with few waves.
+// and 4-slice batches; the same with 2-slice batches for P <= 2; 8 elements
+// per lane and 16-slice batches for levels with few waves.  TR = groups of 4
+// wave tiles per workgroup, processed as one pipelined sequence.
+#ifndef ZQ_REDUCE_TR
+#define ZQ_REDUCE_TR 1
+#endif
+#ifndef ZQ_REDUCE_TR2
+#define ZQ_REDUCE_TR2 2
+#endif
+#ifndef ZQ_REDUCE_TR_SMALL
+#define ZQ_REDUCE_TR_SMALL 1
+#endif
 enum class ReduceShape { kLarge, kTwoSlices, kSmall };
 constexpr int reduce_elems(ReduceShape s) { return s == ReduceShape::kSmall ? 8 : 32; }
-constexpr int reduce_tiles(ReduceShape s) { return s == ReduceShape::kTwoSlices ? 2 : 1; }
+constexpr int reduce_tiles(ReduceShape s) {
+  return s == ReduceShape::kTwoSlices ? ZQ_REDUCE_TR2 : s == ReduceShape::kSmall ? ZQ_REDUCE_TR_SMALL : ZQ_REDUCE_TR;
+}
 // A level whose E = 32 launch would have fewer waves than this runs the small
 // variant (4x the waves, more slices in flight per wave).
 #ifndef ZQ_REDUCE_SMALL_WAVES

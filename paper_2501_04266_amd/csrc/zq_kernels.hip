@@ -61,6 +61,16 @@
 #ifndef ZQ_REDUCE_U_SMALL
 #define ZQ_REDUCE_U_SMALL 16
 #endif
+// batch pipelining (see the reduce kernel) per launch shape: large / P <= 2 / small
+#ifndef ZQ_REDUCE_PIPE
+#define ZQ_REDUCE_PIPE 1
+#endif
+#ifndef ZQ_REDUCE_PIPE2
+#define ZQ_REDUCE_PIPE2 1
+#endif
+#ifndef ZQ_REDUCE_PIPE_SMALL
+#define ZQ_REDUCE_PIPE_SMALL 0
+#endif
 
 namespace zq {
 namespace {
@@ -273,7 +283,6 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
   else static_cast<uint16_t*>(p)[i] = (uint16_t)f2h(v);
 }
 
-__device__ __forceinline__ int64_t wave_id() { return (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); }
 
 }  // namespace
 
@@ -462,12 +471,21 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
 }
 
 // ------------------------------------------------------------------ reduce level
-// Vector path: slices 16-byte aligned (m % 32 == 0), full blocks only.  A lane
-// owns E consecutive elements (E/2 bytes of every slice: consecutive lanes
-// read consecutive bytes); L = B/E lanes hold one block.  Large levels use
-// E = 32 (16 B per slice per lane) with U = 4 slices loaded ahead; small levels
-// (few waves, often many slices) use E = 8 with U = 16, so four times as many
-// waves run and each has 16 slices in flight instead of 4.
+// Vector path: slices 16-byte aligned (m % 32 == 0), blocks [0, nfull) with
+// nfull a multiple of the group size GB below.  A lane owns E consecutive
+// elements (E/2 bytes of every slice: consecutive lanes read consecutive
+// bytes); L = B/E lanes hold one block; a wave tile is 64 lanes = BPW blocks.
+// The 4 waves of a workgroup take 4 adjacent tiles (a group of GB blocks) and
+// workgroup g processes groups g*TR .. g*TR + TR - 1.  Every load and store is
+// addressed from a wave-uniform base plus the lane's offset, with no
+// predicates.  Large levels use E = 32 (16 B per slice per lane), small levels
+// (few waves, often many slices) E = 8, so that four times as many waves run.
+//
+// Slices are loaded U at a time (a batch).  With PIPE the batches of a
+// workgroup's groups form one sequence of jobs whose register buffers
+// alternate, so the loads of the next batch -- of this tile or of the next
+// group -- are in flight while the current one is summed or the tile
+// requantised; without it each batch is loaded, then summed.
 //
 // Per slice and element: one v_cvt_off_f32_i4 (q/16), one multiply by 16*s
 // ((q/16)*(16 s) is the exact real q*s, so the rounded product is fl(q*s)),
@@ -476,42 +494,51 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
 // first slice initialises the sum with its product: +0 + x = x for every x
 // but -0, and a -0 sum and a +0 sum requantise to the same code and scale.
 // Slices are summed in ascending order, exactly as defined.
-
+//
 // YDT >= 0 adds the fused final dequantisation: the requantised codes are
 // turned back into fl(code * s_out) in YDT (the value qgz_dequantize would
 // produce from this level's output) and written to y; out / sout may then be
 // null, in which case the INT4 result is not stored.  Outputs wider than 16
-// bytes per lane are staged in LDS and written as wave-contiguous 16-byte
-// stores, as in the dequantiser.
+// bytes per lane are staged in LDS and written as workgroup-contiguous
+// 16-byte stores, as in the dequantiser.
 
-template <int B, int E, int U, int TR, int YDT>
+template <int U, int NW>
+struct SliceBatch {
+  uint32_t w[U][NW];
+  float s[U];
+};
+
+template <int B, int E, int U, int TR, bool PIPE, int YDT>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
                                                      float* __restrict__ sout, void* __restrict__ y) {
-  constexpr int L = B / E, BPW = 64 / L, NW = E / 8;  // NW words of nibbles per slice per lane
+  constexpr int L = B / E, BPW = 64 / L, NW = E / 8, WPG = kThreads / 64, GB = WPG * BPW;
   static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4) && TR >= 1, "lane layout");
   constexpr int YB = YDT < 0 ? 0 : E * elem_size<(YDT < 0 ? 0 : YDT)>();  // dequantised bytes per lane
-  constexpr bool YSTAGE = YB > 16 && TR == 1;
+  constexpr bool YSTAGE = YB > 16;
   __shared__ u32x4 ybuf[YSTAGE ? kThreads * YB / 16 : 1];
   const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane_byte = lane * (E / 2);
 
-  uint32_t w[U][NW];
-  float s[U];
-  // loads of slices [p0, p0 + U) of the tile starting at block blk (lane's block)
-  auto load_batch = [&](int64_t blk, int p0) {
-    const bool valid = blk < nfull;
-    const int64_t byte0 = (blk * B + (int64_t)(lane % L) * E) >> 1;
+  const int64_t g0 = (int64_t)blockIdx.x * TR;  // first group of this workgroup
+  const int64_t groups = nfull / GB;
+  const int ng = (int)(groups - g0 >= TR ? TR : groups - g0);  // >= 1 by the launch size
+  const int nb = (P + U - 1) / U;
+  auto tile_blk0 = [&](int64_t grp) { return (grp * WPG + wv) * BPW; };
+
+  // slices [b*U, b*U + U) of this wave's tile of group grp
+  auto issue = [&](SliceBatch<U, NW>& X, int64_t grp, int b) {
+    const int64_t blk0 = tile_blk0(grp);
+    const uint8_t* tb = in + blk0 * (B / 2);
+    const float* sb = sin + blk0;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int p = p0 + u;
-      if (valid && p < P) {
-        load_words<ZQ_NT_REDUCE, NW>(in + byte0 + (int64_t)p * slice_bytes, w[u]);
-        s[u] = ld<ZQ_NT_REDUCE>(sin + blk + (int64_t)p * slice_scales);
-      } else {
-#pragma unroll
-        for (int j = 0; j < NW; ++j) w[u][j] = 0u;
-        s[u] = 0.0f;
+      const int p = b * U + u;
+      if (p < P) {
+        load_words<ZQ_NT_REDUCE, NW>(tb + (int64_t)p * slice_bytes + lane_byte, X.w[u]);
+        X.s[u] = ld<ZQ_NT_REDUCE>(sb + (int64_t)p * slice_scales + lane / L);
       }
     }
   };
@@ -544,29 +571,17 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
       }
     }
   };
-
-  const int64_t wave0 = wave_id() * TR;
-  load_batch(wave0 * BPW + lane / L, 0);
-#pragma unroll 1
-  for (int t = 0; t < TR; ++t) {
-    const int64_t blk = (wave0 + t) * BPW + lane / L;
-    const bool valid = blk < nfull;
-    const int64_t e0 = blk * B + (int64_t)(lane % L) * E;
-    const int64_t byte0 = e0 >> 1;
-    for (int p0 = 0; p0 < P; p0 += U) {
-      if (p0 > 0) load_batch(blk, p0);
-      if (p0 == 0) {
-        accumulate(w[0], s[0], true);
-      } else {
-        accumulate(w[0], s[0], false);
-      }
+  auto sum_batch = [&](const SliceBatch<U, NW>& X, int b) {
+    if (b == 0) accumulate(X.w[0], X.s[0], true);
+    else accumulate(X.w[0], X.s[0], false);
 #pragma unroll
-      for (int u = 1; u < U; ++u)
-        if (p0 + u < P) accumulate(w[u], s[u], false);
-    }
-    // next tile's first batch goes out before this tile's requantisation
-    if (t + 1 < TR) load_batch(blk + BPW, 0);
+    for (int u = 1; u < U; ++u)
+      if (b * U + u < P) accumulate(X.w[u], X.s[u], false);
+  };
 
+  // requantise this wave's tile of group grp and store it
+  auto finish = [&](int64_t grp) {
+    const int64_t blk0 = tile_blk0(grp);
     float a = fabsf(acc[0]);
 #pragma unroll
     for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
@@ -579,28 +594,73 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
     uint32_t m[E];
 #pragma unroll
     for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
-    if (out != nullptr && valid) {
+    if (out != nullptr) {
       uint32_t o[NW];
 #pragma unroll
       for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
-      store_words<ZQ_NT_REDUCE, NW>(out + byte0, o);
-      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk, so);
+      store_words<ZQ_NT_REDUCE, NW>(out + blk0 * (B / 2) + lane_byte, o);
+      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk0 + lane / L, so);
     }
     if constexpr (YDT >= 0) {
       // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
       float v[E];
 #pragma unroll
       for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
-      const int64_t wg_blk0 = (int64_t)blockIdx.x * (kThreads / 64) * BPW;
-      if (YSTAGE && wg_blk0 + (kThreads / 64) * BPW <= nfull) {  // workgroup-uniform
+      if constexpr (YSTAGE) {  // every wave of the workgroup is here, at the same group
         store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
         __syncthreads();
-        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + wg_blk0 * B * elem_size<YDT>());
+        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + grp * GB * B * elem_size<YDT>());
 #pragma unroll
         for (int c = 0; c < YB / 16; ++c)
           st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
-      } else if (valid) {
-        store_elems<ZQ_NT_DEQ4, YDT, E>(y, e0, v);
+        __syncthreads();
+      } else {
+        store_elems<ZQ_NT_DEQ4, YDT, E>(y, blk0 * B + (int64_t)lane * E, v);
+      }
+    }
+  };
+
+  SliceBatch<U, NW> A;
+  if constexpr (!PIPE) {
+#pragma unroll 1
+    for (int t = 0; t < ng; ++t) {
+#pragma unroll 1
+      for (int b = 0; b < nb; ++b) {
+        issue(A, g0 + t, b);
+        sum_batch(A, b);
+      }
+      finish(g0 + t);
+    }
+  } else {
+    // jobs (group g0 + t, batch b) in order, two buffers alternating
+    SliceBatch<U, NW> Bf;
+    const int njobs = ng * nb;
+    int it = 0, ib = 0, ct = 0, cb = 0;  // next job to issue / to consume
+    auto next = [&](int& t, int& b) {
+      if (++b == nb) {
+        b = 0;
+        ++t;
+      }
+    };
+    issue(A, g0 + it, ib);
+    next(it, ib);
+#pragma unroll 1
+    for (int j = 0; j < njobs; j += 2) {
+      if (j + 1 < njobs) {
+        issue(Bf, g0 + it, ib);
+        next(it, ib);
+      }
+      sum_batch(A, cb);
+      if (cb == nb - 1) finish(g0 + ct);
+      next(ct, cb);
+      if (j + 2 < njobs) {
+        issue(A, g0 + it, ib);
+        next(it, ib);
+      }
+      if (j + 1 < njobs) {
+        sum_batch(Bf, cb);
+        if (cb == nb - 1) finish(g0 + ct);
+        next(ct, cb);
       }
     }
   }
@@ -728,18 +788,21 @@ static ReduceKernel reduce_kernel_for(int lgB, ReduceShape shape) {
   // next tile's loads issued before this tile's requantisation; small: E = 8,
   // U = 16.  A block may span at most one wave, so B = 1024 always takes large.
   constexpr int EL = kReduceElems, UL = ZQ_REDUCE_U, ES = kReduceElemsSmall, US = ZQ_REDUCE_U_SMALL;
+  constexpr int TL = reduce_tiles(ReduceShape::kLarge), T2 = reduce_tiles(ReduceShape::kTwoSlices),
+                TS = reduce_tiles(ReduceShape::kSmall);
+  constexpr bool PL = ZQ_REDUCE_PIPE, P2 = ZQ_REDUCE_PIPE2, PS = ZQ_REDUCE_PIPE_SMALL;
 #define ZQ_REDUCE_CASE(LG, BB)                                                                       \
   case LG:                                                                                           \
-    if (shape == ReduceShape::kSmall) return &k_reduce<BB, ES, US, 1, YDT>;                          \
-    if (shape == ReduceShape::kTwoSlices) return &k_reduce<BB, EL, 2, 2, YDT>;                       \
-    return &k_reduce<BB, EL, UL, 1, YDT>;
+    if (shape == ReduceShape::kSmall) return &k_reduce<BB, ES, US, TS, PS, YDT>;                     \
+    if (shape == ReduceShape::kTwoSlices) return &k_reduce<BB, EL, 2, T2, P2, YDT>;                  \
+    return &k_reduce<BB, EL, UL, TL, PL, YDT>;
   switch (lgB) {
     ZQ_REDUCE_CASE(5, 32)
     ZQ_REDUCE_CASE(6, 64)
     ZQ_REDUCE_CASE(7, 128)
     ZQ_REDUCE_CASE(8, 256)
     ZQ_REDUCE_CASE(9, 512)
-    default: return &k_reduce<1024, EL, UL, 1, YDT>;
+    default: return &k_reduce<1024, EL, UL, TL, PL, YDT>;
   }
 #undef ZQ_REDUCE_CASE
 }
