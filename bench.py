@@ -446,6 +446,28 @@ def main():
                         "fused_bytes": fused_bytes,
                         "fused_GBps": round(fused_bytes / (times["fused"] * 1e-6) / 1e9, 1)}
 
+    # all-shares mode of the P=8 level: 8 slices of the whole layer (m = n),
+    # random INT4 codes and scales, for a bandwidth figure over 2.17 GB
+    pin = torch.from_numpy(wl.random_bytes(8 * nb4(n), key=[3, wl.ROLE_MISC, 9, 0])).to("cuda")
+    sin = torch.from_numpy(wl.uniform_f32(8 * nsc(n, GBLOCK), *wl.ALL_SHARES_SCALES,
+                                          key=[3, wl.ROLE_MISC, 9, 1])).to("cuda")
+    aop = torch.empty(nb4(n), dtype=torch.uint8, device="cuda")
+    aos = torch.empty(nsc(n, GBLOCK), dtype=torch.float32, device="cuda")
+    allsh = lambda: zq.qgz_reduce_level(pin, sin, 8, n, GBLOCK, packed_out=aop, scales_out=aos)
+    for _ in range(3):
+        allsh()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        allsh()
+    e1.record()
+    torch.cuda.synchronize()
+    as_us = e0.elapsed_time(e1) * 1e3 / args.steps
+    as_bytes = bytes_reduce(8, n, GBLOCK)
+    all_shares = {"qgz_reduce_level P=8 m=n us": round(as_us, 2), "bytes": as_bytes,
+                  "GBps": round(as_bytes / (as_us * 1e-6) / 1e9, 1)}
+    del pin, sin, aop, aos
+
     # next row: the degree-2 weight partition (1/2 shard quantised into its slot
     # of the gathered buffer; the dequantisation of the gathered layer is the
     # same call as in the step)
@@ -496,6 +518,7 @@ def main():
         "kernels": kernels,
         "fused_last_level": fused,
         "sec_degree_2": sec_degree_2,
+        "all_shares": all_shares,
         "copy_ceiling_GBps": round(copy_gbps, 1),
     }
 

@@ -67,6 +67,29 @@ def normal_f32(n, std, key):
     return _fill(out, key, draw)
 
 
+def random_bytes(nbytes, key):
+    """Uniform random bytes (uint8), deterministic in `key`.  As packed INT4
+    slices these are codes uniform over all 16 nibble values."""
+    out = np.empty(nbytes, np.uint8)
+
+    def draw(g, o):
+        o[:] = np.frombuffer(g.bytes(o.size), np.uint8)
+
+    return _fill(out, key, draw)
+
+
+def uniform_f32(n, lo, hi, key):
+    """float32 uniform in [lo, hi), n elements, deterministic in `key`."""
+    out = np.empty(n, np.float32)
+
+    def draw(g, o):
+        g.random(o.size, dtype=np.float32, out=o)
+        o *= np.float32(hi - lo)
+        o += np.float32(lo)
+
+    return _fill(out, key, draw)
+
+
 def to_storage(x32, dtype):
     """Round a float32 array to the storage dtype, nearest-even.
     Returns float32 / float16 arrays, or uint16 bit patterns for bf16."""
@@ -119,6 +142,9 @@ N_TINY = 1024 * 1024
 N_13B = layer_params(2048)      # 50,331,648
 N_20B = layer_params(6144)      # 452,984,832
 N_EDGE = 123_456_789
+# scales of the random all-shares slices: the range of absmax/7 over blocks of
+# 128 elements of an N(0, 1e-3) gradient is about [3e-4, 8e-4]
+ALL_SHARES_SCALES = (2e-4, 1e-3)
 
 CONFIGS = {
     1: dict(name="tiny-1024x1024", n=N_TINY, wdtype="f16", wblock=256, shard=1, qwz_out="f16",

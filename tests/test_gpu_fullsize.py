@@ -12,6 +12,8 @@ inputs (the oracle is fast enough to compute whole tensors).
   4  GPT-20B layer, three levels P = 2, 4, 48, final dequant to fp32
   5  123,456,789-element fp32 stress tensor (Student-t nu=3 x0.02, 0.1% x100
      outliers, zero groups), INT8 B=256 and INT4 B=64, dequant to bf16
+  all-shares mode of the reduce level (m = n): P = 2 at config 1's size,
+     P = 8 over the whole GPT-20B layer
 """
 import numpy as np
 import pytest
@@ -130,6 +132,28 @@ def test_config3_gpt20b_layer_gradients():
 
 def test_config4_gpt20b_three_levels():
     _qgz_chain_case(4, wl.N_20B, [2, 4, 48], 128, "f32")
+
+
+def _all_shares_case(cfg, P, m, block):
+    """All-shares mode of a reduce level: P slices of the whole tensor (m = n),
+    random INT4 codes (all 16 nibble values) and scales in the range an
+    N(0, 1e-3) gradient gives."""
+    pin = wl.random_bytes(P * _nb4(m), key=[cfg, wl.ROLE_MISC, 9, 0])
+    sin = wl.uniform_f32(P * _nsc(m, block), *wl.ALL_SHARES_SCALES, key=[cfg, wl.ROLE_MISC, 9, 1])
+    rp, rs = zq.qgz_reduce_level(torch.from_numpy(pin).cuda(), torch.from_numpy(sin).cuda(), P, m, block)
+    torch.cuda.synchronize()
+    orp, ors = oracle.qgz_reduce_level(pin, sin, P, m, block)
+    assert_bits_equal(from_dev(rp), orp, f"cfg{cfg} all-shares P={P} packed", block // 2)
+    assert_bits_equal(from_dev(rs), ors, f"cfg{cfg} all-shares P={P} scales")
+
+
+def test_config1_all_shares():
+    _all_shares_case(1, 2, wl.N_TINY, 128)
+
+
+def test_config3_all_shares_p8():
+    """P = 8 slices of the whole GPT-20B layer (2.17 GB moved)."""
+    _all_shares_case(3, 8, wl.N_20B, 128)
 
 
 @pytest.mark.parametrize("variant", ["int8-b256", "int4-b64"])
