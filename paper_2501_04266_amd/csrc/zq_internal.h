@@ -68,7 +68,7 @@ constexpr int kReduceElemsSmall = 8;  // 4 bytes per slice per lane, for small l
 #define ZQ_REDUCE_TR_SMALL 1
 #endif
 enum class ReduceShape { kLarge, kTwoSlices, kSmall };
-constexpr int reduce_elems(ReduceShape s) { return s == ReduceShape::kSmall ? 8 : 32; }
+constexpr int reduce_elems(ReduceShape s) { return s == ReduceShape::kSmall ? kReduceElemsSmall : kReduceElems; }
 constexpr int reduce_tiles(ReduceShape s) {
   return s == ReduceShape::kTwoSlices ? ZQ_REDUCE_TR2 : s == ReduceShape::kSmall ? ZQ_REDUCE_TR_SMALL : ZQ_REDUCE_TR;
 }

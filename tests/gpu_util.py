@@ -36,7 +36,16 @@ def bits(a):
 
 
 def empty(n, dtype):
-    return torch.empty(n, dtype=_TORCH[dtype], device=DEV)
+    return poisoned(n, _TORCH[dtype])
+
+
+def poisoned(n, dtype):
+    """Output buffer filled with 0xA5 bytes: a region a kernel fails to write
+    cannot match the expected values by accident."""
+    t = torch.empty(n, dtype=dtype, device=DEV)
+    if n:
+        t.view(torch.uint8).fill_(0xA5)
+    return t
 
 
 def assert_bits_equal(got, want, what, block=None):

@@ -22,7 +22,7 @@ import torch
 import oracle
 import paper_2501_04266_amd as zq
 from paper_2501_04266_amd import workloads as wl
-from tests.gpu_util import assert_bits_equal, from_dev, to_dev
+from tests.gpu_util import assert_bits_equal, from_dev, poisoned, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -42,8 +42,8 @@ def _qwz_case(cfg, x, dtype, block, shard, out):
     dequantise the whole gathered layer, as the bench step does."""
     n = x.size
     xd = to_dev(x, dtype)
-    codes = torch.empty(n, dtype=torch.int8, device="cuda")
-    scales = torch.empty(_nsc(n, block), dtype=torch.float32, device="cuda")
+    codes = poisoned(n, torch.int8)
+    scales = poisoned(_nsc(n, block), torch.float32)
     zq.qwz_quantize(xd, block, codes=codes, scales=scales)          # gathered layer (all shards)
     s = n // shard
     zq.qwz_quantize(xd[:s], block, codes=codes[:s], scales=scales[:_nsc(s, block)])

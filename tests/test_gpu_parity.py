@@ -14,7 +14,7 @@ import torch
 import oracle
 import paper_2501_04266_amd as zq
 from tests import pin_checks as pc
-from tests.gpu_util import assert_bits_equal, from_dev, to_dev
+from tests.gpu_util import assert_bits_equal, from_dev, poisoned, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -310,8 +310,8 @@ def test_reduce_dequantize_fused(P, block, m, out):
     y = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt)
     torch.cuda.synchronize()
     assert_bits_equal(from_dev(y), want, f"fused P={P} B={block} m={m} -> {out}")
-    gp = torch.empty(zq.int4_bytes(m), dtype=torch.uint8, device="cuda")
-    gs = torch.empty(zq.num_scales(m, block), dtype=torch.float32, device="cuda")
+    gp = poisoned(zq.int4_bytes(m), torch.uint8)
+    gs = poisoned(zq.num_scales(m, block), torch.float32)
     y2 = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt, packed_out=gp, scales_out=gs)
     torch.cuda.synchronize()
     assert_bits_equal(from_dev(y2), want, "fused (with INT4 output)")
@@ -348,12 +348,12 @@ def test_hip_graph_capture_replays():
     x_host = (g.standard_normal(n) * 1e-3).astype(np.float32)
     x = to_dev(x_host)
     P, m = 4, n // 4
-    packed = torch.empty(n // 2, dtype=torch.uint8, device="cuda")
-    scales = torch.empty(n // block, dtype=torch.float32, device="cuda")
-    rp = torch.empty(m // 2, dtype=torch.uint8, device="cuda")
-    rs = torch.empty(m // block, dtype=torch.float32, device="cuda")
-    y = torch.empty(m, dtype=torch.float32, device="cuda")
-    yf = torch.empty(m, dtype=torch.bfloat16, device="cuda")
+    packed = poisoned(n // 2, torch.uint8)
+    scales = poisoned(n // block, torch.float32)
+    rp = poisoned(m // 2, torch.uint8)
+    rs = poisoned(m // block, torch.float32)
+    y = poisoned(m, torch.float32)
+    yf = poisoned(m, torch.bfloat16)
 
     def path():
         zq.qgz_quantize(x, block, packed=packed, scales=scales)
