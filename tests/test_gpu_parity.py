@@ -186,6 +186,11 @@ for P in (1, 2, 3, 4, 8, 48):
 for P, block, m in ((3, 128, (1 << 23) + 4096), (2, 64, (1 << 23) + 2048), (2, 256, (1 << 24) + 256),
                     (1, 128, (1 << 23) + 4096), (2, 32, (1 << 22) + 1024)):
     REDUCE_CASES.append((P, block, m))
+# batches that do not divide P (odd job counts in the pipelined kernel), and
+# the largest P the ABI accepts, on the small-level and the generic path
+for P, block, m in ((5, 128, (1 << 23) + 4096), (9, 64, 1 << 23), (17, 128, 4096 * 8),
+                    (1024, 128, 8192), (1024, 64, 1000)):
+    REDUCE_CASES.append((P, block, m))
 # ragged m: not a multiple of the block, of 32, odd
 for P, block, m in ((2, 128, 1000), (3, 64, 999), (8, 128, 65536 + 77), (48, 64, 4095), (5, 1024, 3000),
                     (4, 32, 33), (2, 256, 1)):
