@@ -127,6 +127,25 @@ int qgz_dequantize(const uint8_t* packed, const float* scales, int64_t n, int32_
 int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
                           void* y, zq_dtype yt, uint8_t* packed_out, float* scales_out, void* stream);
 
+/* Dequantise-on-load GEMM: the forward product of a layer whose weight
+ * arrives as the gathered INT8 buffer (Design, Weight Partitioning: the
+ * Allgathered weights are dequantised for the forward pass), without writing
+ * the dequantised weight to memory:
+ *   y[m][n] = sum_k x[m][k] * w[n][k],  w[n][k] = cvt(fl(q[n*K + k] * s[(n*K + k) / block]))
+ * i.e. w is exactly what qwz_dequantize(codes, scales, N*K, block, ., xt)
+ * writes, and the sum is taken in binary32 by the matrix cores in an order of
+ * their own (not bit-reproducible against another order; within
+ * 2*K*2^-24 * sum_k |x[m][k] w[n][k]| of the exact value).
+ *   x       [M][K] row-major, xt = ZQ_BF16 or ZQ_F16 (read)
+ *   codes   [N][K] int8 row-major (a PyTorch Linear weight, flattened), scales
+ *           [ceil(N*K/block)] floats (read)
+ *   y       [M][N] float row-major (written)
+ * K must be a multiple of 64 (ZQ_E_SIZE otherwise); M, N >= 0 arbitrary; K = 0
+ * writes zeros.  x and codes 16-byte aligned, scales and y 4-byte aligned; y
+ * must not overlap an input.  Other conventions as above. */
+int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,
+                     int64_t K, int32_t block, float* y, void* stream);
+
 /* Size helpers (host only): number of scales ceil(n/block) (-1 on a bad
  * block or n < 0), and INT4 bytes ceil(n/2) (-1 for n < 0). */
 int64_t zq_num_scales(int64_t n, int32_t block);

@@ -9,6 +9,10 @@ numpy arrays: float32, float16, or uint16 holding bfloat16 bit patterns
 (pass dtype="bf16" for those).  The method, and every reading taken where the
 paper is silent, is documented in zq_oracle.c.
 
+`qwz_dequant_gemm` is the forward product of a layer whose weight is held as
+the gathered INT8 buffer: dequantise (this package's qwz_dequantize), then one
+float64 matrix product.
+
 The 3-level chain (`chain`) composes reduce levels the way the paper's
 hierarchical partitioning stacks them (Design: weights over a GCD pair,
 gradients over a node, optimizer states over all ranks): level k receives P_k
@@ -197,3 +201,32 @@ def f32_to_bf16_bits(v):
 
 def f16_bits_to_f32(h):
     return _load().zqo_f16_to_f32(int(h))
+
+
+def elements_to_f64(a, dtype):
+    """float32 / float16 arrays, or uint16 bfloat16 bit patterns, widened to
+    float64 exactly."""
+    if dtype == "bf16":
+        return (np.asarray(a, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    return np.asarray(a).astype(np.float64)
+
+
+def qwz_dequant_gemm(x, codes, scales, N, block, dtype="bf16"):
+    """Forward product of a layer whose weight arrives as the gathered INT8
+    buffer (Design, Weight Partitioning: the Allgathered weight is dequantised
+    for the forward pass): y = x @ W^T.  W is the N x K weight in PyTorch Linear
+    layout, W[n][k] = element n*K + k of qwz_dequantize(codes, scales, block,
+    dtype); x is [M, K] of dtype (bf16 as uint16 bit patterns).  Returns y as
+    float64 [M, N].
+
+    The steps are the definition as written: dequantise, then one float64
+    matrix product.  Each product of two bf16 / fp16 values is exact in
+    float64; the float64 sum is within K * 2^-53 * sum_k |x w| of the exact
+    value, far inside the binary32-accumulation bound (2 K 2^-24 sum_k |x w|)
+    a GPU result is held to."""
+    x = np.asarray(x)
+    M, K = x.shape
+    w = qwz_dequantize(np.asarray(codes)[:N * K], scales, block, dtype)
+    W = elements_to_f64(w, dtype).reshape(N, K)
+    X = elements_to_f64(x, dtype).reshape(M, K)
+    return X @ W.T

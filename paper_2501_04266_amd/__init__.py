@@ -17,6 +17,7 @@ from ._lib import (  # noqa: F401
     qgz_quantize,
     qgz_reduce_dequantize,
     qgz_reduce_level,
+    qwz_dequant_gemm,
     qwz_dequantize,
     qwz_quantize,
 )

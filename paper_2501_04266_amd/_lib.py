@@ -17,7 +17,7 @@ ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
 STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",
           -5: "ZQ_E_SIZE", -6: "ZQ_E_P", -7: "ZQ_E_HIP", -8: "ZQ_E_ALIAS"}
 EXPORTS = ["qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-           "qgz_reduce_dequantize", "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
+           "qgz_reduce_dequantize", "qwz_dequant_gemm", "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
 
 _TORCH_DT = {torch.float32: ZQ_F32, torch.float16: ZQ_F16, torch.bfloat16: ZQ_BF16}
 _DT_TORCH = {v: k for k, v in _TORCH_DT.items()}
@@ -46,6 +46,7 @@ def lib():
         "qgz_dequantize": [vp, vp, i64, i32, vp, ci, vp],
         "qgz_reduce_level": [vp, vp, i32, i64, i32, vp, vp, vp],
         "qgz_reduce_dequantize": [vp, vp, i32, i64, i32, vp, ci, vp, vp, vp],
+        "qwz_dequant_gemm": [vp, ci, vp, vp, i64, i64, i64, i32, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -157,4 +158,22 @@ def qgz_reduce_dequantize(packed_in, scales_in, P, m, block=128, out_dtype=torch
                                        None if packed_out is None else _dev(packed_out, "packed_out"),
                                        None if scales_out is None else _dev(scales_out, "scales_out"),
                                        _stream(stream)), "qgz_reduce_dequantize")
+    return y
+
+
+def qwz_dequant_gemm(x, codes, scales, N, block=256, y=None, stream=None):
+    """y[M, N] = x[M, K] @ deq(W)^T with W the N x K INT8 weight (codes int8
+    [N*K] row-major, scales [ceil(N*K/block)]) dequantised to x's dtype
+    (bf16 or fp16) on load; y is float32.  K must be a multiple of 64."""
+    if x.dim() != 2:
+        raise ValueError("x must be 2-D [M, K]")
+    M, K = x.shape
+    if codes.numel() < N * K or scales.numel() < num_scales(N * K, block):
+        raise ValueError("codes / scales smaller than an N x K weight")
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float32, device=x.device)
+    if x.dtype not in (torch.bfloat16, torch.float16) or y.dtype != torch.float32:
+        raise TypeError("x must be bf16 or fp16 and y float32")
+    _check(lib().qwz_dequant_gemm(_dev(x, "x"), _TORCH_DT[x.dtype], _dev(codes, "codes"), _dev(scales, "scales"),
+                                  M, N, K, block, _dev(y, "y"), _stream(stream)), "qwz_dequant_gemm")
     return y

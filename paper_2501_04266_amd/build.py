@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libzq.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("zq_kernels.hip", "zq_api.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("zq_kernels.hip", "zq_gemm.hip", "zq_api.hip")]
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",

@@ -229,6 +229,24 @@ int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int3
   return reduce(packed_in, scales_in, P, m, block, packed_out, scales_out, true, y, yt, stream);
 }
 
+int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,
+                     int64_t K, int32_t block, float* y, void* stream) {
+  if (M < 0 || N < 0 || K < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (xt != ZQ_BF16 && xt != ZQ_F16) return ZQ_E_DTYPE;
+  if (K % kDqGemmK != 0) return ZQ_E_SIZE;
+  if (M == 0 || N == 0) return ZQ_OK;
+  if (!y || (K > 0 && (!x || !codes || !scales))) return ZQ_E_NULL;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, 4)) return ZQ_E_ALIGN;
+  if (any_overlap({{y, 4 * M * N}}, {{x, 2 * M * K}, {codes, N * K}, {scales, 4 * num_scales(N * K, block)}}))
+    return ZQ_E_ALIAS;
+  const int64_t mtiles = (M + kDqGemmTile - 1) / kDqGemmTile, ntiles = (N + kDqGemmTile - 1) / kDqGemmTile;
+  if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
+  return launch(dqgemm_kernel(xt), (unsigned)(mtiles * ntiles), kDqGemmThreads, static_cast<hipStream_t>(stream),
+                static_cast<const uint16_t*>(x), codes, scales, M, N, K, lgB, y, mtiles, ntiles);
+}
+
 int64_t zq_num_scales(int64_t n, int32_t block) {
   if (n < 0 || log2_block(block) < 0) return -1;
   return num_scales(n, block);

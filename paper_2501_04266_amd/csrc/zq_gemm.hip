@@ -1,0 +1,197 @@
+// zq_gemm.hip -- dequantise-on-load GEMM for gfx950 MFMA.
+//
+// The gathered INT8 layer feeds the forward matmuls of that layer (the paper's
+// Design, Weight Partitioning: the Allgathered weights are dequantised for the
+// forward pass).  Instead of writing the dequantised bf16 / fp16 layer to HBM
+// and reading it back in the matmul, this kernel dequantises each weight tile
+// as it is staged into LDS:
+//
+//   y[m][n] = sum_k x[m][k] * w[n][k],   w[n][k] = cvt(fl(q[n*K + k] * s[(n*K + k) / B]))
+//
+// with q / s the qwZ codes and block scales of the N x K weight (PyTorch
+// Linear layout, flat row-major) and cvt the nearest-even narrowing to x's
+// type -- exactly the values qwz_dequantize writes.  Products are exact in
+// binary32 and summed in binary32 by the MFMA units (v_mfma_f32_32x32x16_bf16
+// / _f16), in an order the hardware fixes.
+//
+// Tiling: a workgroup of 4 waves computes a 128 x 128 tile of y, each wave a
+// 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  K advances 64 at a time:
+// the next x tile (16 B per load) and code tile (16 codes and their scale per
+// load) are fetched into registers while the MFMAs run on the current LDS
+// buffer, then dequantised and stored into the other buffer.  LDS rows are
+// padded by 16 bytes so the 16-byte fragment reads of 8 consecutive lanes fall
+// in distinct banks.  Workgroups are numbered so that each XCD receives a
+// contiguous range of tiles, and within it groups of 8 tile rows share their
+// weight tiles through that XCD's L2.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "zq.h"
+#include "zq_device.h"
+#include "zq_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace zq {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kLDK = kBK + 8;  // LDS row stride in 16-bit elements (144 bytes)
+constexpr int kGemmThreads = 256;
+constexpr int kGroupM = 8;     // tile rows sharing a weight tile in L2
+constexpr int kXcds = 8;
+
+template <int XT>
+__device__ __forceinline__ f32x16_t mfma32(u32x4 a, u32x4 b, f32x16_t c) {
+  if constexpr (XT == ZQ_BF16)
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
+                                                  0, 0, 0);
+}
+
+// two binary32 values narrowed to XT, packed low-first
+template <int XT>
+__device__ __forceinline__ uint32_t narrow2(float a, float b) {
+  if constexpr (XT == ZQ_BF16) return bf16x2_bits(a, b);
+  else return f2h(a) | (f2h(b) << 16);
+}
+
+template <int XT>
+__global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+                                                         const float* __restrict__ scales, int64_t M, int64_t N,
+                                                         int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
+                                                         int64_t ntiles) {
+  __shared__ u32x4 As[2][kBM * kLDK / 8];
+  __shared__ u32x4 Bs[2][kBN * kLDK / 8];
+
+  // workgroup -> tile: XCD-contiguous ranges (workgroups are dealt to the
+  // XCDs round robin), then column-major groups of kGroupM tile rows
+  const int64_t T = mtiles * ntiles;
+  const int64_t q = T / kXcds, r = T % kXcds, xcd = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
+  const int64_t t = xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int64_t per_group = (int64_t)kGroupM * ntiles;
+  const int64_t first_m = (t / per_group) * kGroupM;
+  const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
+  const int64_t mt = first_m + (t % per_group) % gsize;
+  const int64_t nt = (t % per_group) / gsize;
+  const int64_t m0 = mt * kBM, n0 = nt * kBN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+  const int KT = (int)(K / kBK);
+
+  u32x4 xr[4], wr[2];
+  float sr[2];
+  // global -> registers: x rows m0.., 8 elements per chunk; codes rows n0..,
+  // 16 codes per chunk with the scale of their block (a chunk never straddles
+  // a block: chunks are 16-aligned in the flat index and B >= 32)
+  auto gload = [&](int kt) {
+    const int64_t k0 = (int64_t)kt * kBK;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + kGemmThreads * i, row = c >> 3, col = (c & 7) * 8;
+      const int64_t m = m0 + row;
+      xr[i] = m < M ? *reinterpret_cast<const u32x4*>(x + m * K + k0 + col) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + kGemmThreads * i, row = c >> 2, col = (c & 3) * 16;
+      const int64_t n = n0 + row;
+      if (n < N) {
+        const int64_t f = n * K + k0 + col;
+        wr[i] = *reinterpret_cast<const u32x4*>(codes + f);
+        sr[i] = scales[f >> lgB];
+      } else {
+        wr[i] = u32x4{0u, 0u, 0u, 0u};
+        sr[i] = 0.0f;
+      }
+    }
+  };
+  // registers -> LDS buffer `buf`; codes become fl(q * s) narrowed to XT
+  auto sstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int c = tid + kGemmThreads * i, row = c >> 3, col = (c & 7) * 8;
+      As[buf][(row * kLDK + col) / 8] = xr[i];
+    }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + kGemmThreads * i, row = c >> 2, col = (c & 3) * 16;
+      uint32_t o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t word = wr[i][j >> 1];
+        const int sh = (j & 1) * 16;
+        const float v0 = (float)(int32_t)(int8_t)(word >> sh) * sr[i];
+        const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * sr[i];
+        o[j] = narrow2<XT>(v0, v1);
+      }
+      Bs[buf][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
+      Bs[buf][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
+    }
+  };
+
+  f32x16_t acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  // MFMA operands: lane l holds row (l % 32) of its 32-row tile, k elements
+  // [8 (l / 32), 8 (l / 32) + 8) of the 16-wide step
+  const int frow = lane & 31, fk = 8 * (lane >> 5);
+  auto compute = [&](int buf) {
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      u32x4 a[2], b[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) a[i] = As[buf][((wm * 64 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+#pragma unroll
+      for (int j = 0; j < 2; ++j) b[j] = Bs[buf][((wn * 64 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<XT>(a[i], b[j], acc[i][j]);
+    }
+  };
+
+  if (KT > 0) {
+    gload(0);
+    sstore(0);
+  }
+  __syncthreads();
+#pragma unroll 1
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) gload(kt + 1);
+    compute(cur);
+    if (kt + 1 < KT) sstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (m < M && n < N) y[m * N + n] = acc[i][j][e];
+      }
+    }
+}
+
+}  // namespace
+
+DqGemmKernel dqgemm_kernel(int xt) { return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16> : &k_dqgemm<ZQ_F16>; }
+
+}  // namespace zq

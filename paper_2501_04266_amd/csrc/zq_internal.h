@@ -92,4 +92,12 @@ DequantKernel dequant_kernel(int dt, int qbits);
 ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
 ReduceGenericKernel reduce_generic_kernel();
 
+// dequantise-on-load GEMM (x of type xt = ZQ_BF16 or ZQ_F16)
+constexpr int kDqGemmTile = 128;  // rows and columns of y per workgroup
+constexpr int kDqGemmK = 64;      // K must be a multiple of this
+constexpr int kDqGemmThreads = 256;
+using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
+                              int64_t, int64_t);
+DqGemmKernel dqgemm_kernel(int xt);
+
 }  // namespace zq

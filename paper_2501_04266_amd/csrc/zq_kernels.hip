@@ -26,6 +26,7 @@
 #include <stdint.h>
 
 #include "zq.h"
+#include "zq_device.h"
 #include "zq_internal.h"
 
 #pragma clang fp contract(off)
@@ -75,8 +76,6 @@
 namespace zq {
 namespace {
 
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kRoundMagic = 12582912.0f;  // 1.5 * 2^23
 constexpr float kFlushBelow = 0x1p-119f;    // absmax below this: zero block
@@ -93,8 +92,6 @@ __device__ __forceinline__ void st(T* p, T v) {
   else *p = v;
 }
 
-__device__ __forceinline__ uint32_t f2u(float f) { return __builtin_bit_cast(uint32_t, f); }
-__device__ __forceinline__ float u2f(uint32_t u) { return __builtin_bit_cast(float, u); }
 
 // fl(fl(v * r) + 1.5*2^23): for |fl(v*r)| < 2^22 the sum lies in [2^23, 2^24)
 // where binary32 spacing is 1, so it is 1.5*2^23 + rint_even(fl(v*r)); the
@@ -210,27 +207,6 @@ __device__ __forceinline__ void store_words(void* p, const uint32_t (&w)[NW]) {
 }
 
 // ------------------------------------------------------------------ element formats
-
-typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
-typedef float f32x2_t __attribute__((ext_vector_type(2)));
-
-// two binary32 -> two bfloat16 (v_cvt_pk_bf16_f32, nearest even)
-__device__ __forceinline__ uint32_t bf16x2_bits(float a, float b) {
-  f32x2_t v = {a, b};
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
-}
-
-__device__ __forceinline__ float h2f(uint32_t bits16) {
-  return (float)__builtin_bit_cast(_Float16, (uint16_t)bits16);
-}
-// binary32 -> binary16, nearest even (v_cvt_f16_f32).  The empty asm pins v
-// as a materialised binary32 value: without it the compiler folds a preceding
-// fp32 multiply and this narrowing into one v_fma_mixlo_f16, which rounds the
-// exact product once instead of rounding it to binary32 first.
-__device__ __forceinline__ uint32_t f2h(float v) {
-  asm("" : "+v"(v));
-  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v);
-}
 
 template <int DT>
 constexpr int elem_size() { return DT == ZQ_F32 ? 4 : 2; }

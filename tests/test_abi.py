@@ -129,3 +129,24 @@ def test_reduce_dequantize_argument_errors(L):
     assert f(vp(A), vp(C), 8, 256, 128, vp(Y), 0, vp(Y + 512), vp(B), None) == -8  # y over packed_out
     # the plain reduce still requires its INT4 outputs
     assert L.qgz_reduce_level(vp(A), vp(C), 8, 256, 128, None, None, None) == -1
+
+
+def test_dequant_gemm_argument_errors(L):
+    f = L.qwz_dequant_gemm
+    vp = ctypes.c_void_p
+    Y = 0x7F0030000000
+    # (x, xt, codes, scales, M, N, K, block, y)
+    assert f(vp(A), 0, vp(B), vp(C), 4, 4, 64, 256, vp(Y), None) == -3      # fp32 x not supported
+    assert f(vp(A), 2, vp(B), vp(C), 4, 4, 96, 256, vp(Y), None) == -5      # K not a multiple of 64
+    assert f(vp(A), 2, vp(B), vp(C), -1, 4, 64, 256, vp(Y), None) == -5
+    assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 100, vp(Y), None) == -2
+    assert f(vp(A), 2, vp(B), vp(C), 0, 4, 64, 256, None, None) == 0        # empty output: no-op
+    assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 256, None, None) == -1
+    assert f(None, 2, vp(B), vp(C), 4, 4, 64, 256, vp(Y), None) == -1
+    assert f(vp(A + 8), 2, vp(B), vp(C), 4, 4, 64, 256, vp(Y), None) == -4
+    assert f(vp(A), 2, vp(B + 4), vp(C), 4, 4, 64, 256, vp(Y), None) == -4
+    assert f(vp(A), 1, vp(B), vp(C), 4, 4, 64, 256, vp(Y + 2), None) == -4
+    # y (4 x 4 floats) over the end of x (4 x 64 bf16 = 512 bytes)
+    assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 256, vp(A + 500), None) == -8
+    # y over the scales
+    assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 256, vp(C), None) == -8

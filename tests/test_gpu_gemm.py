@@ -1,0 +1,123 @@
+"""GPU parity of the dequantise-on-load GEMM (qwz_dequant_gemm) with the
+oracle.  Two kinds of cases:
+
+* exact: x small multiples of 1/4, scales 2^-7 (so every dequantised weight
+  q/128 is exact in bf16 / fp16) -- every partial sum is a multiple of 2^-9
+  below 2^15, exact in binary32 in any order, so the result must equal the
+  oracle's bit for bit;
+* realistic: x ~ N(0, 1), weights N(0, 0.02) quantised by the oracle; the
+  binary32 sum in the matrix cores' order is held to
+  |y - exact| <= 2 K 2^-24 sum_k |x w| (+ 2^-126 for underflow), the bound for
+  any order of K - 1 rounded binary32 additions of exact products.
+Plus the layer's four GEMMs (GPT-20B, 8192 tokens) on sampled rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2501_04266_amd as zq
+from paper_2501_04266_amd import workloads as wl
+from tests.gpu_util import from_dev, poisoned, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _x_dev(x, dtype):
+    return to_dev(x, dtype).reshape(x.shape)
+
+
+def _exact_inputs(M, N, K, B, dtype, seed):
+    rng = np.random.default_rng(seed)
+    xf = (rng.integers(-16, 17, (M, K)) / 4.0).astype(np.float32)
+    x = wl.to_storage(xf.reshape(-1), dtype).reshape(M, K)
+    codes = rng.integers(-127, 128, N * K).astype(np.int8)
+    scales = np.full(-(-(N * K) // B), 2.0 ** -7, np.float32)
+    return x, codes, scales
+
+
+EXACT = [(1, 1, 64, 256), (37, 100, 192, 32), (128, 128, 64, 256), (300, 257, 1024, 128), (129, 383, 640, 64),
+         (256, 512, 6144, 256)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K,B", EXACT)
+def test_dequant_gemm_exact(M, N, K, B, dtype):
+    x, codes, scales = _exact_inputs(M, N, K, B, dtype, M * 7 + N + K)
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, dtype)
+    y = zq.qwz_dequant_gemm(_x_dev(x, dtype), to_dev(codes), to_dev(scales), N, B)
+    torch.cuda.synchronize()
+    got = from_dev(y).astype(np.float64)
+    assert got.shape == (M, N)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
+
+
+def _check_bound(got, x, codes, scales, N, B, dtype, what):
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, dtype)
+    K = x.shape[1]
+    wdq = oracle.elements_to_f64(oracle.qwz_dequantize(codes[:N * K], scales, B, dtype), dtype).reshape(N, K)
+    mag = np.abs(oracle.elements_to_f64(x, dtype).reshape(x.shape)) @ np.abs(wdq).T
+    tol = 2.0 * K * 2.0 ** -24 * mag + 2.0 ** -126
+    err = np.abs(got.astype(np.float64) - want)
+    worst = np.unravel_index(np.argmax(err - tol), err.shape)
+    assert np.all(err <= tol), f"{what}: error {err[worst]:.3e} > bound {tol[worst]:.3e} at {worst}"
+    return float((err / np.maximum(mag, 1e-300)).max())
+
+
+REAL = [(256, 384, 6144, 256), (100, 130, 1024, 64), (64, 256, 24576, 256), (1, 128, 64, 32)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K,B", REAL)
+def test_dequant_gemm_realistic(M, N, K, B, dtype):
+    xf = wl.normal_f32(M * K, 1.0, key=[8, wl.ROLE_MISC, M, K])
+    x = wl.to_storage(xf, dtype).reshape(M, K)
+    w = wl.weights(N * K, "f32", key=[8, wl.ROLE_WEIGHT, N, K])
+    codes, scales = oracle.qwz_quantize(w, B, "f32")
+    y = zq.qwz_dequant_gemm(_x_dev(x, dtype), to_dev(codes), to_dev(scales), N, B)
+    torch.cuda.synchronize()
+    _check_bound(from_dev(y), x, codes, scales, N, B, dtype, f"M={M} N={N} K={K} B={B} {dtype}")
+
+
+def test_dequant_gemm_k_zero_and_empty():
+    x = torch.zeros((5, 0), dtype=torch.bfloat16, device="cuda")
+    codes = torch.zeros(16, dtype=torch.int8, device="cuda")
+    scales = torch.zeros(1, dtype=torch.float32, device="cuda")
+    y = poisoned(5 * 7, torch.float32).reshape(5, 7)
+    zq.qwz_dequant_gemm(x, codes, scales, 7, 256, y=y)
+    torch.cuda.synchronize()
+    assert bool((y == 0).all())
+    x0 = torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda")
+    assert zq.qwz_dequant_gemm(x0, codes, scales, 0, 256).shape == (0, 0)
+
+
+def test_dequant_gemm_rejects_ragged_k():
+    x = torch.zeros((4, 96), dtype=torch.bfloat16, device="cuda")
+    codes = torch.zeros(4 * 96, dtype=torch.int8, device="cuda")
+    scales = torch.zeros(2, dtype=torch.float32, device="cuda")
+    with pytest.raises(zq.ZQError):
+        zq.qwz_dequant_gemm(x, codes, scales, 4, 256)
+
+
+def test_gpt20b_layer_gemms_sampled_rows():
+    """The four forward GEMMs of the GPT-20B layer (QKV 3h x h, attention out
+    h x h, FC1 4h x h, FC2 h x 4h; h = 6144) over 8192 tokens, weights taken
+    from the gathered INT8 layer at their offsets; 24 sampled rows of each
+    output against the oracle (the launch configuration the bench times)."""
+    h, M, B = 6144, 8192, 256
+    w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
+    codes, scales = oracle.qwz_quantize(w, B, "bf16")
+    del w
+    dcodes, dscales = to_dev(codes), to_dev(scales)
+    rows = np.unique(np.concatenate([[0, M - 1], np.random.default_rng(9).integers(0, M, 22)]))
+    off = 0
+    for name, N, K in (("qkv", 3 * h, h), ("attn_out", h, h), ("fc1", 4 * h, h), ("fc2", h, 4 * h)):
+        xf = wl.normal_f32(M * K, 1.0, key=[8, wl.ROLE_MISC, 1, K])
+        x = wl.to_storage(xf, "bf16").reshape(M, K)
+        y = zq.qwz_dequant_gemm(_x_dev(x, "bf16"), dcodes[off:off + N * K], dscales[off // B:(off + N * K) // B],
+                                N, B)
+        torch.cuda.synchronize()
+        got = from_dev(y[torch.from_numpy(rows).cuda()])
+        _check_bound(got, x[rows], codes[off:off + N * K], scales[off // B:(off + N * K) // B], N, B, "bf16", name)
+        off += N * K
