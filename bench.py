@@ -326,6 +326,68 @@ def load_valu(call):
     return None
 
 
+GEMM_TOKENS = 8192
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def gemm_figures(L, reps, log):
+    """The GPT-20B layer's four forward GEMMs (QKV 3h x h, attention out h x h,
+    FC1 4h x h, FC2 h x 4h) over GEMM_TOKENS rows of bf16 activations, weights
+    from the gathered INT8 layer: fused dequantise-on-load vs qwz_dequantize of
+    the layer followed by torch's bf16 GEMM (hipBLASLt)."""
+    import torch
+    import torch.nn.functional as F
+    zq = L.zq
+    h, M, B = 6144, GEMM_TOKENS, WBLOCK
+    shapes = (("qkv", 3 * h, h), ("attn_out", h, h), ("fc1", 4 * h, h), ("fc2", h, 4 * h))
+    g = torch.Generator(device="cuda")
+    g.manual_seed(20250104)
+    xs = {K: torch.randn((M, K), device="cuda", dtype=torch.bfloat16, generator=g) for K in (h, 4 * h)}
+    ys = {name: torch.empty((M, N), device="cuda", dtype=torch.float32) for name, N, _ in shapes}
+    slices = []
+    off = 0
+    for name, N, K in shapes:
+        slices.append((name, N, K, L.codes[off:off + N * K], L.wscales[off // B:(off + N * K) // B]))
+        off += N * K
+
+    def fused():
+        for name, N, K, c, sc in slices:
+            zq.qwz_dequant_gemm(xs[K], c, sc, N, B, y=ys[name])
+
+    def separate():
+        zq.qwz_dequantize(L.codes, L.wscales, B, y=L.y)
+        o = 0
+        for name, N, K, _, _ in slices:
+            F.linear(xs[K], L.y[o:o + N * K].view(N, K))
+            o += N * K
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    flops = sum(2 * M * N * K for _, N, K in shapes)
+    f_ms, s_ms = timed(fused), timed(separate)
+    per = {}
+    for name, N, K, c, sc in slices:
+        ms = timed(lambda: zq.qwz_dequant_gemm(xs[K], c, sc, N, B, y=ys[name]))
+        per[name] = round(2 * M * N * K / (ms * 1e-3) / 1e12, 1)
+    tf = flops / (f_ms * 1e-3) / 1e12
+    log(f"dequant GEMM: fused {f_ms:.3f} ms ({tf:.0f} TFLOP/s), separate {s_ms:.3f} ms")
+    return {"tokens": M, "flops": flops, "fused_ms": round(f_ms, 3), "fused_TFLOPs": round(tf, 1),
+            "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+            "per_gemm_TFLOPs": per,
+            "separate_dequant_plus_torch_gemm_ms": round(s_ms, 3),
+            "separate_TFLOPs": round(flops / (s_ms * 1e-3) / 1e12, 1)}
+
+
 def cpu_model():
     try:
         for ln in open("/proc/cpuinfo"):
@@ -345,6 +407,7 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
     ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
     ap.add_argument("--no-single-thread", action="store_true", help="skip the 1-thread oracle step")
+    ap.add_argument("--steps-gemm", type=int, default=10, help="timed repetitions of the layer's GEMMs")
     ap.add_argument("--n", type=int, default=0, help=argparse.SUPPRESS)  # smaller layer for quick checks
     args = ap.parse_args()
 
@@ -486,6 +549,11 @@ def main():
     sec_degree_2 = {"qwz_quantize half-shard us": round(sd2_us, 2), "bytes": sd2_bytes,
                     "GBps": round(sd2_bytes / (sd2_us * 1e-6) / 1e9, 1)}
 
+    # next row: the layer's forward GEMMs with the gathered INT8 weight
+    # dequantised on load (qwz_dequant_gemm), 8192 tokens of bf16 activations,
+    # against dequantising the layer to bf16 and running torch's GEMM on it
+    dq_gemm = gemm_figures(L, args.steps_gemm, log)
+
     # practical ceiling: a plain device-to-device copy of 1 GiB
     src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     dst = torch.empty_like(src)
@@ -519,6 +587,7 @@ def main():
         "fused_last_level": fused,
         "sec_degree_2": sec_degree_2,
         "all_shares": all_shares,
+        "dequant_gemm": dq_gemm,
         "copy_ceiling_GBps": round(copy_gbps, 1),
     }
 

@@ -241,7 +241,7 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, 4)) return ZQ_E_ALIGN;
   if (any_overlap({{y, 4 * M * N}}, {{x, 2 * M * K}, {codes, N * K}, {scales, 4 * num_scales(N * K, block)}}))
     return ZQ_E_ALIAS;
-  const int64_t mtiles = (M + kDqGemmTile - 1) / kDqGemmTile, ntiles = (N + kDqGemmTile - 1) / kDqGemmTile;
+  const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
   if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
   return launch(dqgemm_kernel(xt), (unsigned)(mtiles * ntiles), kDqGemmThreads, static_cast<hipStream_t>(stream),
                 static_cast<const uint16_t*>(x), codes, scales, M, N, K, lgB, y, mtiles, ntiles);

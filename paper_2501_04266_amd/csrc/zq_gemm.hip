@@ -14,15 +14,16 @@
 // binary32 and summed in binary32 by the MFMA units (v_mfma_f32_32x32x16_bf16
 // / _f16), in an order the hardware fixes.
 //
-// Tiling: a workgroup of 4 waves computes a 128 x 128 tile of y, each wave a
-// 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32.  K advances 64 at a time:
-// the next x tile (16 B per load) and code tile (16 codes and their scale per
-// load) are fetched into registers while the MFMAs run on the current LDS
-// buffer, then dequantised and stored into the other buffer.  LDS rows are
-// padded by 16 bytes so the 16-byte fragment reads of 8 consecutive lanes fall
-// in distinct banks.  Workgroups are numbered so that each XCD receives a
-// contiguous range of tiles, and within it groups of 8 tile rows share their
-// weight tiles through that XCD's L2.
+// Tiling: a workgroup of 8 waves computes a 256 x 256 tile of y, each wave a
+// 128 x 64 block as 4 x 2 MFMA tiles of 32 x 32 (other shapes are template
+// parameters).  K advances 64 at a time: the next x tile (16 B per load) and
+// code tile (16 codes and their scale per load) are fetched into registers
+// while the MFMAs run on the current LDS buffer, then dequantised and stored
+// into the other buffer.  LDS rows are padded by 16 bytes so the 16-byte
+// fragment reads of 8 consecutive lanes fall in distinct banks.  Workgroups
+// are numbered so that each XCD receives a contiguous range of tiles, and
+// within it groups of 8 tile rows share their weight tiles through that XCD's
+// L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -39,9 +40,8 @@ typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kBK = 64;
 constexpr int kLDK = kBK + 8;  // LDS row stride in 16-bit elements (144 bytes)
-constexpr int kGemmThreads = 256;
 constexpr int kGroupM = 8;     // tile rows sharing a weight tile in L2
 constexpr int kXcds = 8;
 
@@ -62,13 +62,21 @@ __device__ __forceinline__ uint32_t narrow2(float a, float b) {
   else return f2h(a) | (f2h(b) << 16);
 }
 
-template <int XT>
-__global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+// BM x BN tile of y per workgroup, WM x WN waves, each wave a (BM/WM) x (BN/WN)
+// block of 32 x 32 MFMA tiles.
+template <int XT, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                          const float* __restrict__ scales, int64_t M, int64_t N,
                                                          int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
                                                          int64_t ntiles) {
-  __shared__ u32x4 As[2][kBM * kLDK / 8];
-  __shared__ u32x4 Bs[2][kBN * kLDK / 8];
+  constexpr int NT = 64 * WM * WN;                         // threads
+  constexpr int TI = BM / WM / 32, TJ = BN / WN / 32;      // MFMA tiles per wave
+  constexpr int XC = BM * kBK / 8 / NT;                    // x chunks (8 elements) per thread
+  constexpr int WC = BN * kBK / 16 / NT;                   // code chunks (16 codes) per thread
+  static_assert(TI >= 1 && TJ >= 1 && XC >= 1 && WC >= 1 && XC * NT * 8 == BM * kBK && WC * NT * 16 == BN * kBK,
+                "tile shape");
+  __shared__ u32x4 As[2][BM * kLDK / 8];
+  __shared__ u32x4 Bs[2][BN * kLDK / 8];
 
   // workgroup -> tile: XCD-contiguous ranges (workgroups are dealt to the
   // XCDs round robin), then column-major groups of kGroupM tile rows
@@ -80,27 +88,27 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
   const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
   const int64_t mt = first_m + (t % per_group) % gsize;
   const int64_t nt = (t % per_group) / gsize;
-  const int64_t m0 = mt * kBM, n0 = nt * kBN;
+  const int64_t m0 = mt * BM, n0 = nt * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
   const int KT = (int)(K / kBK);
 
-  u32x4 xr[4], wr[2];
-  float sr[2];
+  u32x4 xr[XC], wr[WC];
+  float sr[WC];
   // global -> registers: x rows m0.., 8 elements per chunk; codes rows n0..,
   // 16 codes per chunk with the scale of their block (a chunk never straddles
   // a block: chunks are 16-aligned in the flat index and B >= 32)
   auto gload = [&](int kt) {
     const int64_t k0 = (int64_t)kt * kBK;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + kGemmThreads * i, row = c >> 3, col = (c & 7) * 8;
+    for (int i = 0; i < XC; ++i) {
+      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
       const int64_t m = m0 + row;
       xr[i] = m < M ? *reinterpret_cast<const u32x4*>(x + m * K + k0 + col) : u32x4{0u, 0u, 0u, 0u};
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + kGemmThreads * i, row = c >> 2, col = (c & 3) * 16;
+    for (int i = 0; i < WC; ++i) {
+      const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
       const int64_t n = n0 + row;
       if (n < N) {
         const int64_t f = n * K + k0 + col;
@@ -115,13 +123,13 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
   // registers -> LDS buffer `buf`; codes become fl(q * s) narrowed to XT
   auto sstore = [&](int buf) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int c = tid + kGemmThreads * i, row = c >> 3, col = (c & 7) * 8;
+    for (int i = 0; i < XC; ++i) {
+      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
       As[buf][(row * kLDK + col) / 8] = xr[i];
     }
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + kGemmThreads * i, row = c >> 2, col = (c & 3) * 16;
+    for (int i = 0; i < WC; ++i) {
+      const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
       uint32_t o[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
@@ -136,11 +144,11 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
     }
   };
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
@@ -150,15 +158,15 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
   auto compute = [&](int buf) {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      u32x4 a[2], b[2];
+      u32x4 a[TI], b[TJ];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) a[i] = As[buf][((wm * 64 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int i = 0; i < TI; ++i) a[i] = As[buf][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
-      for (int j = 0; j < 2; ++j) b[j] = Bs[buf][((wn * 64 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int j = 0; j < TJ; ++j) b[j] = Bs[buf][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = mfma32<XT>(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32<XT>(a[i], b[j], acc[i][j]);
     }
   };
 
@@ -178,13 +186,13 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
 
   // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t n = n0 + wn * 64 + j * 32 + (lane & 31);
+    for (int j = 0; j < TJ; ++j) {
+      const int64_t n = n0 + wn * TJ * 32 + j * 32 + (lane & 31);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t m = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int64_t m = m0 + wm * TI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (m < M && n < N) y[m * N + n] = acc[i][j][e];
       }
     }
@@ -192,6 +200,11 @@ __global__ void __launch_bounds__(kGemmThreads) k_dqgemm(const uint16_t* __restr
 
 }  // namespace
 
-DqGemmKernel dqgemm_kernel(int xt) { return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16> : &k_dqgemm<ZQ_F16>; }
+static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads, "launch shape");
+
+DqGemmKernel dqgemm_kernel(int xt) {
+  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>
+                       : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>;
+}
 
 }  // namespace zq

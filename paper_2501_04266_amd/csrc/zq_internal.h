@@ -93,9 +93,22 @@ ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
 ReduceGenericKernel reduce_generic_kernel();
 
 // dequantise-on-load GEMM (x of type xt = ZQ_BF16 or ZQ_F16)
-constexpr int kDqGemmTile = 128;  // rows and columns of y per workgroup
-constexpr int kDqGemmK = 64;      // K must be a multiple of this
-constexpr int kDqGemmThreads = 256;
+#ifndef ZQ_GEMM_BM
+#define ZQ_GEMM_BM 256
+#endif
+#ifndef ZQ_GEMM_BN
+#define ZQ_GEMM_BN 256
+#endif
+#ifndef ZQ_GEMM_WM
+#define ZQ_GEMM_WM 2
+#endif
+#ifndef ZQ_GEMM_WN
+#define ZQ_GEMM_WN 4
+#endif
+constexpr int kDqGemmTileM = ZQ_GEMM_BM;  // rows of y per workgroup
+constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
+constexpr int kDqGemmK = 64;              // K must be a multiple of this
+constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
 using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
                               int64_t, int64_t);
 DqGemmKernel dqgemm_kernel(int xt);
