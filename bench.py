@@ -27,6 +27,10 @@ roofline figure).  Events between launches cost GPU time, so the step time
 is never taken from the breakdown pass.
 
 Output: one JSON line.  value = algorithmic bytes of the step / step time.
+Extra fields, measured after the timed region: the last level fused with the
+final dequantisation, the degree-2 weight shard, the P = 8 level in
+all-shares mode (m = n), and the layer's forward GEMMs with the INT8 weight
+dequantised on load (8192 tokens) against dequantise + torch's GEMM.
 """
 import argparse
 import json
