@@ -134,8 +134,10 @@ int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int3
  *   y[m][n] = sum_k x[m][k] * w[n][k],  w[n][k] = cvt(fl(q[n*K + k] * s[(n*K + k) / block]))
  * i.e. w is exactly what qwz_dequantize(codes, scales, N*K, block, ., xt)
  * writes, and the sum is taken in binary32 by the matrix cores in an order of
- * their own (not bit-reproducible against another order; within
- * 2*K*2^-24 * sum_k |x[m][k] w[n][k]| of the exact value).
+ * their own, always within 2*K*2^-24 * sum_k |x[m][k] w[n][k]| of the exact
+ * value.  For M <= 512 the K range may be split across workgroups whose
+ * partial sums are added into y atomically (after the library zeroes y), so
+ * such results can differ between runs in their last bits.
  *   x       [M][K] row-major, xt = ZQ_BF16 or ZQ_F16 (read)
  *   codes   [N][K] int8 row-major (a PyTorch Linear weight, flattened), scales
  *           [ceil(N*K/block)] floats (read)

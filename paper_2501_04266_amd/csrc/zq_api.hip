@@ -241,10 +241,31 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
   if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, 4)) return ZQ_E_ALIGN;
   if (any_overlap({{y, 4 * M * N}}, {{x, 2 * M * K}, {codes, N * K}, {scales, 4 * num_scales(N * K, block)}}))
     return ZQ_E_ALIAS;
-  const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
-  if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
-  return launch(dqgemm_kernel(xt), (unsigned)(mtiles * ntiles), kDqGemmThreads, static_cast<hipStream_t>(stream),
-                static_cast<const uint16_t*>(x), codes, scales, M, N, K, lgB, y, mtiles, ntiles);
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint16_t* xh = static_cast<const uint16_t*>(x);
+  if (M > ZQ_GEMM_SMALL_M) {
+    const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
+    if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
+    return launch(dqgemm_kernel(xt, false, false), (unsigned)(mtiles * ntiles), kDqGemmThreads, st, xh, codes,
+                  scales, M, N, K, lgB, y, mtiles, ntiles, 1);
+  }
+  // few rows: small tiles, and K split across workgroups (partial tiles added
+  // into a zeroed y) when the tiles alone cannot fill the GPU
+  const int64_t mtiles = (M + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
+  const int64_t ntiles = (N + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
+  const int64_t tiles = mtiles * ntiles, ksteps = K / kDqGemmK;
+  int64_t splits = (kDqGemmSplitTarget + tiles - 1) / tiles;
+  if (splits > ksteps) splits = ksteps;
+  if (splits < 1) splits = 1;
+  if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
+  if (splits == 1)
+    return launch(dqgemm_kernel(xt, true, false), (unsigned)tiles, kDqGemmSmallThreads, st, xh, codes, scales, M, N,
+                  K, lgB, y, mtiles, ntiles, 1);
+  const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
+  int rc = launch(fill_zero_kernel(), (unsigned)fill_grid, 256u, st, y, count);
+  if (rc != ZQ_OK) return rc;
+  return launch(dqgemm_kernel(xt, true, true), (unsigned)(tiles * splits), kDqGemmSmallThreads, st, xh, codes,
+                scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
 }
 
 int64_t zq_num_scales(int64_t n, int32_t block) {

@@ -64,11 +64,14 @@ __device__ __forceinline__ uint32_t narrow2(float a, float b) {
 
 // BM x BN tile of y per workgroup, WM x WN waves, each wave a (BM/WM) x (BN/WN)
 // block of 32 x 32 MFMA tiles.
-template <int XT, int BM, int BN, int WM, int WN>
+// SPLIT: workgroup w takes K-steps [s KT / splits, (s + 1) KT / splits) of
+// tile w / splits (s = w % splits) and adds its partial tile into y, which the
+// host has zeroed; used when there are too few tiles to fill the GPU.
+template <int XT, int BM, int BN, int WM, int WN, bool SPLIT>
 __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                          const float* __restrict__ scales, int64_t M, int64_t N,
                                                          int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
-                                                         int64_t ntiles) {
+                                                         int64_t ntiles, int splits) {
   constexpr int NT = 64 * WM * WN;                         // threads
   constexpr int TI = BM / WM / 32, TJ = BN / WN / 32;      // MFMA tiles per wave
   constexpr int XC = BM * kBK / 8 / NT;                    // x chunks (8 elements) per thread
@@ -81,8 +84,9 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   // workgroup -> tile: XCD-contiguous ranges (workgroups are dealt to the
   // XCDs round robin), then column-major groups of kGroupM tile rows
   const int64_t T = mtiles * ntiles;
-  const int64_t q = T / kXcds, r = T % kXcds, xcd = blockIdx.x % kXcds, idx = blockIdx.x / kXcds;
-  const int64_t t = xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int64_t wg = SPLIT ? blockIdx.x / splits : blockIdx.x;
+  const int64_t q = T / kXcds, r = T % kXcds, xcd = wg % kXcds, idx = wg / kXcds;
+  const int64_t t = SPLIT ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
   const int64_t per_group = (int64_t)kGroupM * ntiles;
   const int64_t first_m = (t / per_group) * kGroupM;
   const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
@@ -91,7 +95,10 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   const int64_t m0 = mt * BM, n0 = nt * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
-  const int KT = (int)(K / kBK);
+  const int KTall = (int)(K / kBK);
+  const int split = SPLIT ? (int)(blockIdx.x % splits) : 0;
+  const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
+  const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
 
   u32x4 xr[XC], wr[WC];
   float sr[WC];
@@ -99,7 +106,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   // 16 codes per chunk with the scale of their block (a chunk never straddles
   // a block: chunks are 16-aligned in the flat index and B >= 32)
   auto gload = [&](int kt) {
-    const int64_t k0 = (int64_t)kt * kBK;
+    const int64_t k0 = (int64_t)(kt0 + kt) * kBK;
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
@@ -193,18 +200,34 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t m = m0 + wm * TI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (m < M && n < N) y[m * N + n] = acc[i][j][e];
+        if (m < M && n < N) {
+          if constexpr (SPLIT) atomicAdd(y + m * N + n, acc[i][j][e]);
+          else y[m * N + n] = acc[i][j][e];
+        }
       }
     }
 }
 
+// y[0, count) = 0 (for the split kernel, which adds into y)
+__global__ void __launch_bounds__(256) k_fill_zero(float* __restrict__ y, int64_t count) {
+  for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) y[i] = 0.0f;
+}
+
 }  // namespace
 
-static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads, "launch shape");
+static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads && 64 * 2 * 2 == kDqGemmSmallThreads, "launch shape");
 
-DqGemmKernel dqgemm_kernel(int xt) {
-  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>
-                       : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>;
+DqGemmKernel dqgemm_kernel(int xt, bool small, bool split) {
+  if (!small)
+    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
+                         : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
+  if (split)
+    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true>
+                         : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true>;
+  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false>
+                       : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false>;
 }
+
+FillZeroKernel fill_zero_kernel() { return &k_fill_zero; }
 
 }  // namespace zq

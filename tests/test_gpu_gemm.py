@@ -65,7 +65,10 @@ def _check_bound(got, x, codes, scales, N, B, dtype, what):
     return float((err / np.maximum(mag, 1e-300)).max())
 
 
-REAL = [(256, 384, 6144, 256), (100, 130, 1024, 64), (64, 256, 24576, 256), (1, 128, 64, 32)]
+# M <= 512 takes the small-tile path, with K split across workgroups when the
+# tiles alone are too few (all of these but the last)
+REAL = [(256, 384, 6144, 256), (100, 130, 1024, 64), (64, 256, 24576, 256), (1, 128, 64, 32),
+        (16, 24576, 6144, 256), (200, 6144, 24576, 256), (257, 640, 1024, 128), (513, 256, 1024, 256)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
