@@ -124,3 +124,27 @@ def test_gpt20b_layer_gemms_sampled_rows():
         got = from_dev(y[torch.from_numpy(rows).cuda()])
         _check_bound(got, x[rows], codes[off:off + N * K], scales[off // B:(off + N * K) // B], N, B, "bf16", name)
         off += N * K
+
+
+@pytest.mark.parametrize("M", [64, 640])
+def test_dequant_gemm_graph_capture(M):
+    """The GEMM (both the few-row split path, which also launches its own
+    zero fill, and the large-tile path) only enqueues kernels, so it replays
+    from a HIP graph; exact inputs make every replay bit-identical."""
+    N, K, B = 384, 2048, 256
+    x, codes, scales = _exact_inputs(M, N, K, B, "bf16", 31 + M)
+    xd, cd, sd = _x_dev(x, "bf16"), to_dev(codes), to_dev(scales)
+    y = poisoned(M * N, torch.float32).reshape(M, N)
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, "bf16")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            zq.qwz_dequant_gemm(xd, cd, sd, N, B, y=y)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        y.fill_(float("nan"))          # eager work between replays
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(from_dev(y).astype(np.float64), want), f"replay {rep}"

@@ -383,3 +383,40 @@ def test_hip_graph_capture_replays():
         torch.cuda.synchronize()
         for t, w in zip((packed, scales, rp, rs, y, yf), want):
             assert from_dev(t).tobytes() == w.tobytes(), f"replay {rep}"
+
+
+def test_concurrent_host_threads_on_separate_streams():
+    """The library keeps no state: calls from several host threads, each on its
+    own stream (default priority), give the oracle's bits."""
+    import threading
+
+    g = np.random.default_rng(23)
+    n, block = (1 << 21) + 96, 128
+    xs = [(g.standard_normal(n) * 10.0 ** -k).astype(np.float32) for k in range(4)]
+    want = [oracle.qgz_quantize(x, block) for x in xs]
+    xds = [to_dev(x) for x in xs]
+    torch.cuda.synchronize()
+    got, errors = [None] * len(xs), []
+
+    def work(i):
+        try:
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(5):
+                    p, sc = zq.qgz_quantize(xds[i], block)
+                    y = zq.qgz_dequantize(p, sc, n, block, out_dtype=torch.float32)
+            s.synchronize()
+            got[i] = (from_dev(p), from_dev(sc), from_dev(y))
+        except Exception as e:  # reported below, on the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(i,)) for i in range(len(xs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for i, (p, sc, y) in enumerate(got):
+        assert_bits_equal(p, want[i][0], f"thread {i} packed", block // 2)
+        assert_bits_equal(sc, want[i][1], f"thread {i} scales")
+        assert_bits_equal(y, oracle.qgz_dequantize(want[i][0], want[i][1], n, block, "f32"), f"thread {i} dequant")
