@@ -16,16 +16,19 @@
 //
 // Tiling: a workgroup of 8 waves computes a 256 x 256 tile of y, each wave a
 // 128 x 64 block as 4 x 2 MFMA tiles of 32 x 32 (other shapes are template
-// parameters).  K advances 64 at a time: the next x tile (16 B per load) and
-// code tile (16 codes and their scale per load) are fetched into registers
-// while the MFMAs run on the current LDS buffer, then dequantised and stored
-// into the other buffer.  LDS rows are padded by 16 bytes so the 16-byte
+// parameters).  K advances 64 at a time.  x tiles (16 B per load) and code
+// tiles (16 codes and their scale per load) are fetched into one of two
+// register sets two K-steps ahead, so a load has a whole K-step of MFMAs to
+// arrive in; at the end of each K-step the next tile is dequantised and
+// stored into the LDS buffer not being read.  LDS rows are padded by 16 bytes so the 16-byte
 // fragment reads of 8 consecutive lanes fall in distinct banks.  Workgroups
 // are numbered so that each XCD receives a contiguous range of tiles, and
 // within it groups of 8 tile rows share their weight tiles through that XCD's
 // L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "zq.h"
 #include "zq_device.h"
@@ -100,12 +103,19 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
   const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
 
-  u32x4 xr[XC], wr[WC];
-  float sr[WC];
+  // RS register sets: with 2, tile t's loads are issued two K-steps before
+  // its LDS store
+  constexpr int RS = ZQ_GEMM_RSETS;
+  u32x4 xrs[RS][XC], wrs[RS][WC];
+  float srs[RS][WC];
   // global -> registers: x rows m0.., 8 elements per chunk; codes rows n0..,
   // 16 codes per chunk with the scale of their block (a chunk never straddles
   // a block: chunks are 16-aligned in the flat index and B >= 32)
-  auto gload = [&](int kt) {
+  auto gload = [&](int kt, auto rs_c) {
+    constexpr int R = decltype(rs_c)::value;
+    u32x4(&xr)[XC] = xrs[R];
+    u32x4(&wr)[WC] = wrs[R];
+    float(&sr)[WC] = srs[R];
     const int64_t k0 = (int64_t)(kt0 + kt) * kBK;
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
@@ -128,7 +138,11 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
     }
   };
   // registers -> LDS buffer `buf`; codes become fl(q * s) narrowed to XT
-  auto sstore = [&](int buf) {
+  auto sstore = [&](int buf, auto rs_c) {
+    constexpr int R = decltype(rs_c)::value;
+    const u32x4(&xr)[XC] = xrs[R];
+    const u32x4(&wr)[WC] = wrs[R];
+    const float(&sr)[WC] = srs[R];
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
@@ -177,18 +191,45 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
     }
   };
 
-  if (KT > 0) {
-    gload(0);
-    sstore(0);
-  }
-  __syncthreads();
-#pragma unroll 1
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
-    compute(cur);
-    if (kt + 1 < KT) sstore(cur ^ 1);
+  using R0 = std::integral_constant<int, 0>;
+  using R1 = std::integral_constant<int, RS - 1>;
+  if constexpr (RS == 1) {
+    if (KT > 0) {
+      gload(0, R0{});
+      sstore(0, R0{});
+    }
     __syncthreads();
+#pragma unroll 1
+    for (int kt = 0; kt < KT; ++kt) {
+      const int cur = kt & 1;
+      if (kt + 1 < KT) gload(kt + 1, R0{});
+      compute(cur);
+      if (kt + 1 < KT) sstore(cur ^ 1, R0{});
+      __syncthreads();
+    }
+  } else {
+    // tile t lives in register set t % 2 from its load (K-step t - 2) to its
+    // store (end of K-step t - 1)
+    if (KT > 0) {
+      gload(0, R0{});
+      sstore(0, R0{});
+    }
+    if (KT > 1) gload(1, R1{});
+    if (KT > 2) gload(2, R0{});
+    __syncthreads();
+#pragma unroll 1
+    for (int kt = 0; kt < KT; kt += 2) {
+      compute(0);                                   // K-step kt (buffer 0)
+      if (kt + 1 < KT) sstore(1, R1{});             // tile kt + 1
+      if (kt + 3 < KT) gload(kt + 3, R1{});
+      __syncthreads();
+      if (kt + 1 < KT) {
+        compute(1);                                 // K-step kt + 1 (buffer 1)
+        if (kt + 2 < KT) sstore(0, R0{});           // tile kt + 2
+        if (kt + 4 < KT) gload(kt + 4, R0{});
+        __syncthreads();
+      }
+    }
   }
 
   // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32

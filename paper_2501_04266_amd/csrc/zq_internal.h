@@ -105,6 +105,9 @@ ReduceGenericKernel reduce_generic_kernel();
 #ifndef ZQ_GEMM_WN
 #define ZQ_GEMM_WN 4
 #endif
+#ifndef ZQ_GEMM_RSETS
+#define ZQ_GEMM_RSETS 2
+#endif
 constexpr int kDqGemmTileM = ZQ_GEMM_BM;  // rows of y per workgroup
 constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
 constexpr int kDqGemmK = 64;              // K must be a multiple of this
