@@ -23,7 +23,7 @@
 // stored into the LDS buffer not being read.  LDS rows are padded by 16 bytes so the 16-byte
 // fragment reads of 8 consecutive lanes fall in distinct banks.  Workgroups
 // are numbered so that each XCD receives a contiguous range of tiles, and
-// within it groups of 8 tile rows share their weight tiles through that XCD's
+// within it groups of 4 tile rows share their weight tiles through that XCD's
 // L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
@@ -45,7 +45,13 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kBK = 64;
 constexpr int kLDK = kBK + 8;  // LDS row stride in 16-bit elements (144 bytes)
-constexpr int kGroupM = 8;     // tile rows sharing a weight tile in L2
+#ifndef ZQ_GEMM_GROUP_M
+#define ZQ_GEMM_GROUP_M 4
+#endif
+#ifndef ZQ_GEMM_XCD_MAP
+#define ZQ_GEMM_XCD_MAP 1
+#endif
+constexpr int kGroupM = ZQ_GEMM_GROUP_M;  // tile rows sharing a weight tile in L2
 constexpr int kXcds = 8;
 
 template <int XT>
@@ -89,7 +95,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   const int64_t T = mtiles * ntiles;
   const int64_t wg = SPLIT ? blockIdx.x / splits : blockIdx.x;
   const int64_t q = T / kXcds, r = T % kXcds, xcd = wg % kXcds, idx = wg / kXcds;
-  const int64_t t = SPLIT ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int64_t t = SPLIT || !ZQ_GEMM_XCD_MAP ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
   const int64_t per_group = (int64_t)kGroupM * ntiles;
   const int64_t first_m = (t / per_group) * kGroupM;
   const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
