@@ -220,13 +220,16 @@ def oracle_step(L, threads, repeats=1):
     w, g = L.host["w"], L.host["g"]
     codes_all, sc_all = oracle.qwz_quantize(w, WBLOCK, "bf16")       # the gathered layer (prep)
     outs, t = {}, 0.0
+    per_call = []
 
     def timed(fn, *a):
         nonlocal t
         t0 = time.perf_counter()
         for _ in range(repeats):
             r = fn(*a)
-        t += (time.perf_counter() - t0) / repeats
+        dt = (time.perf_counter() - t0) / repeats
+        t += dt
+        per_call.append(round(dt, 4))
         return r
 
     outs["shard_codes"] = timed(oracle.qwz_quantize, w[:s], WBLOCK, "bf16")
@@ -254,6 +257,7 @@ def oracle_step(L, threads, repeats=1):
         cur_m = m
     outs["final"] = timed(oracle.qgz_dequantize, cur_p, cur_s, cur_m, GBLOCK, "f32")
     outs["gp"] = (gp, gs)
+    outs["per_call_s"] = per_call
     return t, outs
 
 
@@ -626,7 +630,8 @@ def main():
         out["cpu_baseline"] = {"value": round(step_bytes / secs / 1e9, 3), "unit": "GB/s", "cores": threads,
                                "kind": "oracle", "seconds_per_step": round(secs, 3), "cpu_model": cpu_model(),
                                "sample": f"the full step of the same workload (all calls, full sizes), each timed "
-                                         f"call repeated {args.cpu_repeats}x, mean"}
+                                         f"call repeated {args.cpu_repeats}x, mean",
+                               "per_call_s": dict(zip([c for c, _, _ in L.calls], outs["per_call_s"]))}
         if threads > 1 and not args.no_single_thread:
             log("oracle step on 1 thread ...")
             secs1, _ = oracle_step(L, 1, 1)
