@@ -80,6 +80,36 @@ def _dev(t, name):
     return t.data_ptr()
 
 
+def _need(t, name, count, dtypes):
+    """Host-side size and dtype check of a caller's buffer: the C ABI takes raw
+    pointers and cannot tell an undersized buffer from a large one."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}; expected one of {[str(d) for d in dtypes]}")
+    if t.numel() < count:
+        raise ValueError(f"{name} holds {t.numel()} elements; {count} needed")
+
+
+def _nsc(n, block):
+    """Scales needed for n elements; 0 for a block the library will reject
+    itself (ZQ_E_BLOCK), so that error is reported as the library's."""
+    if not isinstance(block, int) or block < 32 or block > 1024 or block & (block - 1):
+        return 0
+    return num_scales(n, block)
+
+
+def _alloc_nsc(n, block):
+    """Scales to allocate for n elements (one for a block the library rejects)."""
+    return _nsc(n, block) if _nsc(n, block) or n == 0 else 1
+
+
+_ELEM = (torch.float32, torch.float16, torch.bfloat16)
+_I8 = (torch.int8,)
+_U8 = (torch.uint8,)
+_F32 = (torch.float32,)
+
+
 def _check(status, what):
     if status != 0:
         raise ZQError(status, what)
@@ -88,10 +118,13 @@ def _check(status, what):
 def qwz_quantize(x, block=256, codes=None, scales=None, stream=None):
     """INT8 block quantisation of x (f32/f16/bf16) -> (codes int8[n], scales f32[ceil(n/B)])."""
     n = x.numel()
+    _need(x, "x", n, _ELEM)
     if codes is None:
         codes = torch.empty(n, dtype=torch.int8, device=x.device)
     if scales is None:
-        scales = torch.empty(num_scales(n, block), dtype=torch.float32, device=x.device)
+        scales = torch.empty(_alloc_nsc(n, block), dtype=torch.float32, device=x.device)
+    _need(codes, "codes", n, _I8)
+    _need(scales, "scales", _nsc(n, block), _F32)
     _check(lib().qwz_quantize(_dev(x, "x"), _TORCH_DT[x.dtype], n, block, _dev(codes, "codes"),
                               _dev(scales, "scales"), _stream(stream)), "qwz_quantize")
     return codes, scales
@@ -101,6 +134,9 @@ def qwz_dequantize(codes, scales, block=256, out_dtype=torch.bfloat16, y=None, n
     n = codes.numel() if n is None else n
     if y is None:
         y = torch.empty(n, dtype=out_dtype, device=codes.device)
+    _need(codes, "codes", n, _I8)
+    _need(scales, "scales", _nsc(n, block), _F32)
+    _need(y, "y", n, _ELEM)
     _check(lib().qwz_dequantize(_dev(codes, "codes"), _dev(scales, "scales"), n, block, _dev(y, "y"),
                                 _TORCH_DT[y.dtype], _stream(stream)), "qwz_dequantize")
     return y
@@ -109,10 +145,13 @@ def qwz_dequantize(codes, scales, block=256, out_dtype=torch.bfloat16, y=None, n
 def qgz_quantize(g, block=128, packed=None, scales=None, stream=None):
     """INT4 block quantisation -> (packed uint8[ceil(n/2)], scales f32[ceil(n/B)])."""
     n = g.numel()
+    _need(g, "g", n, _ELEM)
     if packed is None:
         packed = torch.empty(int4_bytes(n), dtype=torch.uint8, device=g.device)
     if scales is None:
-        scales = torch.empty(num_scales(n, block), dtype=torch.float32, device=g.device)
+        scales = torch.empty(_alloc_nsc(n, block), dtype=torch.float32, device=g.device)
+    _need(packed, "packed", int4_bytes(n), _U8)
+    _need(scales, "scales", _nsc(n, block), _F32)
     _check(lib().qgz_quantize(_dev(g, "g"), _TORCH_DT[g.dtype], n, block, _dev(packed, "packed"),
                               _dev(scales, "scales"), _stream(stream)), "qgz_quantize")
     return packed, scales
@@ -121,6 +160,9 @@ def qgz_quantize(g, block=128, packed=None, scales=None, stream=None):
 def qgz_dequantize(packed, scales, n, block=128, out_dtype=torch.float32, y=None, stream=None):
     if y is None:
         y = torch.empty(n, dtype=out_dtype, device=packed.device)
+    _need(packed, "packed", int4_bytes(n), _U8)
+    _need(scales, "scales", _nsc(n, block), _F32)
+    _need(y, "y", n, _ELEM)
     _check(lib().qgz_dequantize(_dev(packed, "packed"), _dev(scales, "scales"), n, block, _dev(y, "y"),
                                 _TORCH_DT[y.dtype], _stream(stream)), "qgz_dequantize")
     return y
@@ -133,9 +175,11 @@ def qgz_reduce_level(packed_in, scales_in, P, m, block=128, packed_out=None, sca
     if packed_out is None:
         packed_out = torch.empty(int4_bytes(m), dtype=torch.uint8, device=dev)
     if scales_out is None:
-        scales_out = torch.empty(num_scales(m, block), dtype=torch.float32, device=dev)
-    if packed_in.numel() < P * int4_bytes(m) or scales_in.numel() < P * num_scales(m, block):
-        raise ValueError("slice buffers smaller than P slices of m elements")
+        scales_out = torch.empty(_alloc_nsc(m, block), dtype=torch.float32, device=dev)
+    _need(packed_in, "packed_in", P * int4_bytes(m), _U8)
+    _need(scales_in, "scales_in", P * _nsc(m, block), _F32)
+    _need(packed_out, "packed_out", int4_bytes(m), _U8)
+    _need(scales_out, "scales_out", _nsc(m, block), _F32)
     _check(lib().qgz_reduce_level(_dev(packed_in, "packed_in"), _dev(scales_in, "scales_in"), P, m, block,
                                   _dev(packed_out, "packed_out"), _dev(scales_out, "scales_out"),
                                   _stream(stream)), "qgz_reduce_level")
@@ -151,8 +195,12 @@ def qgz_reduce_dequantize(packed_in, scales_in, P, m, block=128, out_dtype=torch
         y = torch.empty(m, dtype=out_dtype, device=packed_in.device)
     if (packed_out is None) != (scales_out is None):
         raise ValueError("give both packed_out and scales_out, or neither")
-    if packed_in.numel() < P * int4_bytes(m) or scales_in.numel() < P * num_scales(m, block):
-        raise ValueError("slice buffers smaller than P slices of m elements")
+    _need(packed_in, "packed_in", P * int4_bytes(m), _U8)
+    _need(scales_in, "scales_in", P * _nsc(m, block), _F32)
+    _need(y, "y", m, _ELEM)
+    if packed_out is not None:
+        _need(packed_out, "packed_out", int4_bytes(m), _U8)
+        _need(scales_out, "scales_out", _nsc(m, block), _F32)
     _check(lib().qgz_reduce_dequantize(_dev(packed_in, "packed_in"), _dev(scales_in, "scales_in"), P, m, block,
                                        _dev(y, "y"), _TORCH_DT[y.dtype],
                                        None if packed_out is None else _dev(packed_out, "packed_out"),
@@ -168,12 +216,12 @@ def qwz_dequant_gemm(x, codes, scales, N, block=256, y=None, stream=None):
     if x.dim() != 2:
         raise ValueError("x must be 2-D [M, K]")
     M, K = x.shape
-    if codes.numel() < N * K or scales.numel() < num_scales(N * K, block):
-        raise ValueError("codes / scales smaller than an N x K weight")
+    _need(x, "x", M * K, (torch.bfloat16, torch.float16))
+    _need(codes, "codes", N * K, _I8)
+    _need(scales, "scales", _nsc(N * K, block), _F32)
     if y is None:
         y = torch.empty((M, N), dtype=torch.float32, device=x.device)
-    if x.dtype not in (torch.bfloat16, torch.float16) or y.dtype != torch.float32:
-        raise TypeError("x must be bf16 or fp16 and y float32")
+    _need(y, "y", M * N, _F32)
     _check(lib().qwz_dequant_gemm(_dev(x, "x"), _TORCH_DT[x.dtype], _dev(codes, "codes"), _dev(scales, "scales"),
                                   M, N, K, block, _dev(y, "y"), _stream(stream)), "qwz_dequant_gemm")
     return y

@@ -150,3 +150,38 @@ def test_dequant_gemm_argument_errors(L):
     assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 256, vp(A + 500), None) == -8
     # y over the scales
     assert f(vp(A), 2, vp(B), vp(C), 4, 4, 64, 256, vp(C), None) == -8
+
+
+def test_binding_rejects_undersized_or_mistyped_buffers():
+    """The C ABI takes raw pointers; the binding checks every buffer's size and
+    dtype on the host before anything reaches the library (CPU tensors are
+    enough: these checks come first)."""
+    import torch
+
+    import paper_2501_04266_amd as zq
+    x = torch.zeros(1000)
+    with pytest.raises(ValueError):
+        zq.qwz_quantize(x, 256, codes=torch.zeros(999, dtype=torch.int8), scales=torch.zeros(4))
+    with pytest.raises(ValueError):
+        zq.qwz_quantize(x, 256, codes=torch.zeros(1000, dtype=torch.int8), scales=torch.zeros(3))
+    with pytest.raises(TypeError):
+        zq.qwz_quantize(x, 256, codes=torch.zeros(1000, dtype=torch.int16), scales=torch.zeros(4))
+    with pytest.raises(TypeError):
+        zq.qwz_quantize(torch.zeros(1000, dtype=torch.int32), 256)
+    with pytest.raises(ValueError):
+        zq.qgz_quantize(x, 128, packed=torch.zeros(499, dtype=torch.uint8), scales=torch.zeros(8))
+    with pytest.raises(ValueError):
+        zq.qgz_dequantize(torch.zeros(500, dtype=torch.uint8), torch.zeros(8), 1000, 128, y=torch.zeros(999))
+    with pytest.raises(ValueError):
+        zq.qgz_reduce_level(torch.zeros(999, dtype=torch.uint8), torch.zeros(16), 2, 1000, 128)
+    with pytest.raises(ValueError):
+        zq.qgz_reduce_level(torch.zeros(1000, dtype=torch.uint8), torch.zeros(16), 2, 1000, 128,
+                            packed_out=torch.zeros(10, dtype=torch.uint8), scales_out=torch.zeros(8))
+    with pytest.raises(ValueError):
+        zq.qgz_reduce_dequantize(torch.zeros(1000, dtype=torch.uint8), torch.zeros(16), 2, 1000, 128,
+                                 y=torch.zeros(999))
+    with pytest.raises(ValueError):
+        zq.qwz_dequant_gemm(torch.zeros((4, 64), dtype=torch.bfloat16), torch.zeros(8 * 64, dtype=torch.int8),
+                            torch.zeros(2), 8, 256, y=torch.zeros((4, 7)))
+    with pytest.raises(TypeError):
+        zq.qwz_dequant_gemm(torch.zeros((4, 64)), torch.zeros(8 * 64, dtype=torch.int8), torch.zeros(2), 8, 256)
