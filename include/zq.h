@@ -127,6 +127,25 @@ int qgz_dequantize(const uint8_t* packed, const float* scales, int64_t n, int32_
 int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
                           void* y, zq_dtype yt, uint8_t* packed_out, float* scales_out, void* stream);
 
+/* Reduce level over slices that are not back to back: the receiver reading
+ * each peer's INT4 chunk where it lies, without first copying the chunks into
+ * one receive buffer (the peer-direct form of the quantised all-to-all
+ * reduce-scatter; Background, ZeRO++; Design, Communication Volume Analysis).
+ * On one GPU the slices are separate device buffers; on a node they can be
+ * the peers' buffers mapped into this GPU's address space.
+ *   packed_slices  device array of P pointers; slice p holds ceil(m/2) bytes
+ *   scale_slices   device array of P pointers; slice p holds ceil(m/block) floats
+ * Same arithmetic, order and output as qgz_reduce_level on the slices laid
+ * out back to back (bit-identical).  The two pointer arrays must be 8-byte
+ * aligned and stay unchanged until the call completes; when m % 32 == 0 each
+ * byte slice must be 16-byte aligned and each scale slice 4-byte aligned.
+ * The library cannot read the device-resident pointers on the host, so only
+ * the arrays themselves are checked against the outputs for overlap; the
+ * slices must not overlap the outputs either.  Other conventions and errors
+ * as qgz_reduce_level. */
+int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P,
+                            int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream);
+
 /* Dequantise-on-load GEMM: the forward product of a layer whose weight
  * arrives as the gathered INT8 buffer (Design, Weight Partitioning: the
  * Allgathered weights are dequantised for the forward pass), without writing

@@ -10,6 +10,7 @@ from ._lib import (  # noqa: F401
     LIB_PATH,
     STATUS,
     ZQError,
+    gather_tables,
     int4_bytes,
     lib,
     num_scales,
@@ -17,6 +18,7 @@ from ._lib import (  # noqa: F401
     qgz_quantize,
     qgz_reduce_dequantize,
     qgz_reduce_level,
+    qgz_reduce_level_gather,
     qwz_dequant_gemm,
     qwz_dequantize,
     qwz_quantize,

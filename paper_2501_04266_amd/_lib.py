@@ -17,7 +17,8 @@ ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
 STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",
           -5: "ZQ_E_SIZE", -6: "ZQ_E_P", -7: "ZQ_E_HIP", -8: "ZQ_E_ALIAS"}
 EXPORTS = ["qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-           "qgz_reduce_dequantize", "qwz_dequant_gemm", "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
+           "qgz_reduce_dequantize", "qgz_reduce_level_gather", "qwz_dequant_gemm", "zq_num_scales",
+           "zq_int4_bytes", "zq_status_string"]
 
 _TORCH_DT = {torch.float32: ZQ_F32, torch.float16: ZQ_F16, torch.bfloat16: ZQ_BF16}
 _DT_TORCH = {v: k for k, v in _TORCH_DT.items()}
@@ -47,6 +48,7 @@ def lib():
         "qgz_reduce_level": [vp, vp, i32, i64, i32, vp, vp, vp],
         "qgz_reduce_dequantize": [vp, vp, i32, i64, i32, vp, ci, vp, vp, vp],
         "qwz_dequant_gemm": [vp, ci, vp, vp, i64, i64, i64, i32, vp, vp],
+        "qgz_reduce_level_gather": [vp, vp, i32, i64, i32, vp, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -207,6 +209,54 @@ def qgz_reduce_dequantize(packed_in, scales_in, P, m, block=128, out_dtype=torch
                                        None if scales_out is None else _dev(scales_out, "scales_out"),
                                        _stream(stream)), "qgz_reduce_dequantize")
     return y
+
+
+def gather_tables(packed_slices, scale_slices):
+    """Device tables (int64 tensors) of the slices' addresses, for
+    qgz_reduce_level_gather; build them once to reuse them, e.g. under graph
+    capture, where the per-call host-to-device copy is not allowed."""
+    dev = packed_slices[0].device
+    tab = torch.tensor([_dev(t, "packed_slices[p]") for t in packed_slices], dtype=torch.int64).to(dev)
+    stab = torch.tensor([_dev(t, "scale_slices[p]") for t in scale_slices], dtype=torch.int64).to(dev)
+    return tab, stab
+
+
+def qgz_reduce_level_gather(packed_slices, scale_slices, m, block=128, packed_out=None, scales_out=None,
+                            stream=None, tables=None):
+    """qgz_reduce_level over P slices held in separate tensors (lists of P
+    uint8 tensors of ceil(m/2) bytes and P float32 tensors of ceil(m/B)
+    scales), read in place through device tables of their addresses (built
+    here, or passed as `tables` from gather_tables).  Bit-identical to
+    qgz_reduce_level on the slices laid out back to back."""
+    P = len(packed_slices)
+    if P != len(scale_slices) or P == 0:
+        raise ValueError("give P >= 1 byte slices and as many scale slices")
+    for p, (a, b) in enumerate(zip(packed_slices, scale_slices)):
+        _need(a, f"packed_slices[{p}]", int4_bytes(m), _U8)
+        _need(b, f"scale_slices[{p}]", _nsc(m, block), _F32)
+    dev = packed_slices[0].device
+    if packed_out is None:
+        packed_out = torch.empty(int4_bytes(m), dtype=torch.uint8, device=dev)
+    if scales_out is None:
+        scales_out = torch.empty(_alloc_nsc(m, block), dtype=torch.float32, device=dev)
+    _need(packed_out, "packed_out", int4_bytes(m), _U8)
+    _need(scales_out, "scales_out", _nsc(m, block), _F32)
+    # the pointer tables live in device memory (the kernel reads them); built
+    # here they are allocated on the current stream and, if the call runs on
+    # another, recorded on it so the allocator keeps them until it finishes
+    if tables is None:
+        tab, stab = gather_tables(packed_slices, scale_slices)
+        if stream is not None and hasattr(stream, "cuda_stream"):
+            tab.record_stream(stream)
+            stab.record_stream(stream)
+    else:
+        tab, stab = tables
+        _need(tab, "tables[0]", P, (torch.int64,))
+        _need(stab, "tables[1]", P, (torch.int64,))
+    _check(lib().qgz_reduce_level_gather(tab.data_ptr(), stab.data_ptr(), P, m, block,
+                                         _dev(packed_out, "packed_out"), _dev(scales_out, "scales_out"),
+                                         _stream(stream)), "qgz_reduce_level_gather")
+    return packed_out, scales_out
 
 
 def qwz_dequant_gemm(x, codes, scales, N, block=256, y=None, stream=None):

@@ -134,8 +134,10 @@ int dequantize(const void* codes, const float* scales, int64_t n, int32_t block,
 // Shared body of qgz_reduce_level (fused = false: INT4 output only, both
 // pointers required) and qgz_reduce_dequantize (fused = true: y of dtype yt
 // required, the INT4 output optional -- both of its pointers or neither).
+// Shared body of the reduce entry points.  gather: packed_in / scales_in are
+// device tables of P slice pointers rather than the slices themselves.
 int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
-           uint8_t* packed_out, float* scales_out, bool fused, void* y, int yt, void* stream) {
+           uint8_t* packed_out, float* scales_out, bool fused, void* y, int yt, void* stream, bool gather = false) {
   if (m < 0) return ZQ_E_SIZE;
   const int lgB = log2_block(block);
   if (lgB < 0) return ZQ_E_BLOCK;
@@ -144,11 +146,14 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
   if (m == 0) return ZQ_OK;
   if (!packed_in || !scales_in || (packed_out == nullptr) != (scales_out == nullptr)) return ZQ_E_NULL;
   if (fused ? y == nullptr : packed_out == nullptr) return ZQ_E_NULL;
-  if (!aligned(packed_in, 16) || !aligned(scales_in, 4)) return ZQ_E_ALIGN;
+  if (gather ? !aligned(packed_in, 8) || !aligned(scales_in, 8) : !aligned(packed_in, 16) || !aligned(scales_in, 4))
+    return ZQ_E_ALIGN;
   if (packed_out && (!aligned(packed_out, 16) || !aligned(scales_out, 4))) return ZQ_E_ALIGN;
   if (fused && !aligned(y, 16)) return ZQ_E_ALIGN;
   const int64_t slice_bytes = (m + 1) / 2, nb = num_scales(m, block);
-  const Range ins[] = {{packed_in, slice_bytes * P}, {scales_in, 4 * nb * P}};
+  // (gathered slices live elsewhere; only their pointer tables are checked)
+  const Range ins[] = {{packed_in, gather ? 8 * (int64_t)P : slice_bytes * P},
+                       {scales_in, gather ? 8 * (int64_t)P : 4 * nb * P}};
   Range outs[3];
   int nouts = 0;
   if (packed_out) {
@@ -179,8 +184,9 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
 
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (groups > 0) {
-    int rc = launch(reduce_kernel(lgB, shape, fused ? yt : -1), (unsigned)grid, kThreads, st, packed_in, scales_in,
-                    (int)P, slice_bytes, nb, nfull, packed_out, scales_out, y);
+    int rc = launch(gather ? reduce_gather_kernel(lgB, shape) : reduce_kernel(lgB, shape, fused ? yt : -1),
+                    (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb, nfull, packed_out,
+                    scales_out, y);
     if (rc != ZQ_OK) return rc;
   }
   // remaining blocks (those after the last whole group, including a short
@@ -188,7 +194,8 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
   // per block
   for (int64_t b0 = nfull; b0 < nb; b0 += (1LL << 30)) {
     const int64_t cnt = (nb - b0) < (1LL << 30) ? (nb - b0) : (1LL << 30);
-    int rc = launch(reduce_generic_kernel(), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes, nb, m,
+    int rc = launch(reduce_generic_kernel(gather), (unsigned)cnt, 64u, st, packed_in, scales_in, (int)P, slice_bytes,
+                    nb, m,
                     (int)block, b0, packed_out, scales_out, fused ? y : nullptr, fused ? yt : 0);
     if (rc != ZQ_OK) return rc;
   }
@@ -227,6 +234,12 @@ int qgz_reduce_level(const uint8_t* packed_in, const float* scales_in, int32_t P
 int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t m, int32_t block,
                           void* y, zq_dtype yt, uint8_t* packed_out, float* scales_out, void* stream) {
   return reduce(packed_in, scales_in, P, m, block, packed_out, scales_out, true, y, yt, stream);
+}
+
+int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P,
+                            int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream) {
+  return reduce(reinterpret_cast<const uint8_t*>(packed_slices), reinterpret_cast<const float*>(scale_slices), P, m,
+                block, packed_out, scales_out, false, nullptr, -1, stream, true);
 }
 
 int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,

@@ -90,7 +90,9 @@ QuantTailKernel quant_tail_kernel(int dt, int qbits);
 DequantKernel dequant_kernel(int dt, int qbits);
 // ydt < 0: INT4 output only; otherwise also the fused dequantisation to ydt
 ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
-ReduceGenericKernel reduce_generic_kernel();
+// slices through device tables of P pointers (bytes, scales); INT4 output only
+ReduceKernel reduce_gather_kernel(int lgB, ReduceShape shape);
+ReduceGenericKernel reduce_generic_kernel(bool gather);
 
 // dequantise-on-load GEMM (x of type xt = ZQ_BF16 or ZQ_F16)
 #ifndef ZQ_GEMM_BM

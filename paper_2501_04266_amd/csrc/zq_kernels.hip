@@ -484,7 +484,10 @@ struct SliceBatch {
   float s[U];
 };
 
-template <int B, int E, int U, int TR, bool PIPE, int YDT>
+// GATHER: the slices are not back to back; `in` and `sin` point to device
+// tables of P slice pointers (bytes, scales) instead, e.g. the peers' send
+// buffers mapped into this GPU's address space.
+template <int B, int E, int U, int TR, bool PIPE, int YDT, bool GATHER = false>
 __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                      int P, int64_t slice_bytes, int64_t slice_scales,
                                                      int64_t nfull, uint8_t* __restrict__ out,
@@ -507,14 +510,21 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   // slices [b*U, b*U + U) of this wave's tile of group grp
   auto issue = [&](SliceBatch<U, NW>& X, int64_t grp, int b) {
     const int64_t blk0 = tile_blk0(grp);
-    const uint8_t* tb = in + blk0 * (B / 2);
-    const float* sb = sin + blk0;
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int p = b * U + u;
       if (p < P) {
-        load_words<ZQ_NT_REDUCE, NW>(tb + (int64_t)p * slice_bytes + lane_byte, X.w[u]);
-        X.s[u] = ld<ZQ_NT_REDUCE>(sb + (int64_t)p * slice_scales + lane / L);
+        const uint8_t* tb;
+        const float* sb;
+        if constexpr (GATHER) {
+          tb = reinterpret_cast<const uint8_t* const*>(in)[p] + blk0 * (B / 2);
+          sb = reinterpret_cast<const float* const*>(sin)[p] + blk0;
+        } else {
+          tb = in + blk0 * (B / 2) + (int64_t)p * slice_bytes;
+          sb = sin + blk0 + (int64_t)p * slice_scales;
+        }
+        load_words<ZQ_NT_REDUCE, NW>(tb + lane_byte, X.w[u]);
+        X.s[u] = ld<ZQ_NT_REDUCE>(sb + lane / L);
       }
     }
   };
@@ -646,6 +656,8 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
 // [blk_begin, blk_begin + gridDim.x).  A lane owns byte j = lane + 64 i of the
 // block (elements 2j, 2j+1), i < B/128 rounded up.  Plain arithmetic, the
 // definition as written: sum from +0, one multiply and one add per slice.
+// GATHER as for k_reduce.
+template <bool GATHER>
 __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict__ in, const float* __restrict__ sin,
                                                        int P, int64_t slice_bytes, int64_t slice_scales, int64_t m,
                                                        int B, int64_t blk_begin, uint8_t* __restrict__ out,
@@ -660,8 +672,9 @@ __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict
 #pragma unroll
   for (int k = 0; k < 2 * MAXI; ++k) acc[k] = 0.0f;
   for (int p = 0; p < P; ++p) {
-    const float s = sin[(int64_t)p * slice_scales + blk];
-    const uint8_t* src = in + (int64_t)p * slice_bytes + (base >> 1);
+    const float s = GATHER ? reinterpret_cast<const float* const*>(sin)[p][blk] : sin[(int64_t)p * slice_scales + blk];
+    const uint8_t* src =
+        (GATHER ? reinterpret_cast<const uint8_t* const*>(in)[p] : in + (int64_t)p * slice_bytes) + (base >> 1);
 #pragma unroll
     for (int i = 0; i < MAXI; ++i) {
       const int j = lane + 64 * i;
@@ -792,6 +805,29 @@ ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt) {
   }
 }
 
-ReduceGenericKernel reduce_generic_kernel() { return &k_reduce_generic; }
+ReduceKernel reduce_gather_kernel(int lgB, ReduceShape shape) {
+  constexpr int EL = kReduceElems, UL = ZQ_REDUCE_U, ES = kReduceElemsSmall, US = ZQ_REDUCE_U_SMALL;
+  constexpr int TL = reduce_tiles(ReduceShape::kLarge), T2 = reduce_tiles(ReduceShape::kTwoSlices),
+                TS = reduce_tiles(ReduceShape::kSmall);
+  constexpr bool PL = ZQ_REDUCE_PIPE, P2 = ZQ_REDUCE_PIPE2, PS = ZQ_REDUCE_PIPE_SMALL;
+#define ZQ_GATHER_CASE(LG, BB)                                                                        \
+  case LG:                                                                                            \
+    if (shape == ReduceShape::kSmall) return &k_reduce<BB, ES, US, TS, PS, -1, true>;                 \
+    if (shape == ReduceShape::kTwoSlices) return &k_reduce<BB, EL, 2, T2, P2, -1, true>;              \
+    return &k_reduce<BB, EL, UL, TL, PL, -1, true>;
+  switch (lgB) {
+    ZQ_GATHER_CASE(5, 32)
+    ZQ_GATHER_CASE(6, 64)
+    ZQ_GATHER_CASE(7, 128)
+    ZQ_GATHER_CASE(8, 256)
+    ZQ_GATHER_CASE(9, 512)
+    default: return &k_reduce<1024, EL, UL, TL, PL, -1, true>;
+  }
+#undef ZQ_GATHER_CASE
+}
+
+ReduceGenericKernel reduce_generic_kernel(bool gather) {
+  return gather ? &k_reduce_generic<true> : &k_reduce_generic<false>;
+}
 
 }  // namespace zq

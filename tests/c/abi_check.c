@@ -156,6 +156,24 @@ int main(void) {
     compare(dy, oy, m * sizeof(float), "final dequant");
     compare(dyf, oy, m * sizeof(float), "fused last level");
     expect_status(qgz_reduce_level(dpin, dsin, 0, m, B, drp, drs, st), ZQ_E_P, "reduce P = 0");
+    /* the same level through device tables of slice pointers */
+    {
+      const uint8_t* hp[3];
+      const float* hs[3];
+      for (int p = 0; p < P; ++p) {
+        hp[p] = dpin + p * mb;
+        hs[p] = dsin + p * ms;
+      }
+      const uint8_t** tp = to_dev(hp, sizeof hp);
+      const float** ts = to_dev(hs, sizeof hs);
+      uint8_t* grp = dev_alloc(mb);
+      float* grs = dev_alloc(ms * sizeof(float));
+      expect_status(qgz_reduce_level_gather(tp, ts, P, m, B, grp, grs, st), ZQ_OK, "qgz_reduce_level_gather");
+      HIP_OK(hipStreamSynchronize(st));
+      compare(grp, orp, mb, "gather packed");
+      compare(grs, ors, ms * sizeof(float), "gather scales");
+      HIP_OK(hipFree((void*)tp)); HIP_OK(hipFree((void*)ts)); HIP_OK(hipFree(grp)); HIP_OK(hipFree(grs));
+    }
     HIP_OK(hipFree(dg)); HIP_OK(hipFree(dq)); HIP_OK(hipFree(dqs)); HIP_OK(hipFree(dpin)); HIP_OK(hipFree(dsin));
     HIP_OK(hipFree(drp)); HIP_OK(hipFree(drs)); HIP_OK(hipFree(dy)); HIP_OK(hipFree(dyf));
     free(pin); free(sin_); free(g); free(orp); free(ors); free(oy); free(oq); free(oqs);

@@ -32,7 +32,8 @@ def L():
 def test_header_declares_the_five_calls():
     names = _declared()
     for fn in ("qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-               "qgz_reduce_dequantize", "zq_num_scales", "zq_int4_bytes", "zq_status_string"):
+               "qgz_reduce_dequantize", "qgz_reduce_level_gather", "qwz_dequant_gemm", "zq_num_scales",
+               "zq_int4_bytes", "zq_status_string"):
         assert fn in names, fn
 
 
@@ -185,3 +186,16 @@ def test_binding_rejects_undersized_or_mistyped_buffers():
                             torch.zeros(2), 8, 256, y=torch.zeros((4, 7)))
     with pytest.raises(TypeError):
         zq.qwz_dequant_gemm(torch.zeros((4, 64)), torch.zeros(8 * 64, dtype=torch.int8), torch.zeros(2), 8, 256)
+
+
+def test_reduce_gather_argument_errors(L):
+    f = L.qgz_reduce_level_gather
+    vp = ctypes.c_void_p
+    T, S = 0x7F0040000000, 0x7F0040001000       # device pointer tables (8-byte aligned)
+    assert f(vp(T), vp(S), 0, 256, 128, vp(B), vp(B + 4096), None) == -6
+    assert f(vp(T), vp(S), 8, 256, 100, vp(B), vp(B + 4096), None) == -2
+    assert f(vp(T), vp(S), 8, -1, 128, vp(B), vp(B + 4096), None) == -5
+    assert f(None, vp(S), 8, 256, 128, vp(B), vp(B + 4096), None) == -1
+    assert f(vp(T + 4), vp(S), 8, 256, 128, vp(B), vp(B + 4096), None) == -4   # table not 8-byte aligned
+    assert f(vp(T), vp(S), 8, 256, 128, vp(T + 32), vp(B + 4096), None) == -8  # output over the table
+    assert f(vp(T), vp(S), 8, 0, 128, None, None, None) == 0
