@@ -29,7 +29,8 @@ is never taken from the breakdown pass.
 Output: one JSON line.  value = algorithmic bytes of the step / step time.
 Extra fields, measured after the timed region: the last level fused with the
 final dequantisation, the degree-2 weight shard, the P = 8 level in
-all-shares mode (m = n), and the layer's forward GEMMs with the INT8 weight
+all-shares mode (m = n) and reading its slices in place from separate
+buffers, and the layer's forward GEMMs with the INT8 weight
 dequantised on load (8192 tokens) against dequantise + torch's GEMM.
 """
 import argparse
@@ -562,6 +563,35 @@ def main():
                   "GBps": round(as_bytes / (as_us * 1e-6) / 1e9, 1)}
     del pin, sin, aop, aos
 
+    # next row: the P=8 level reading its slices in place from 8 separate
+    # buffers through device pointer tables (how a receiver would read peers'
+    # send buffers mapped over xGMI) against the contiguous receive buffer
+    mb8, ms8 = nb4(L.m8), nsc(L.m8, GBLOCK)
+    gp_sl = [L.d8[0][p * mb8:(p + 1) * mb8].clone() for p in range(8)]
+    gs_sl = [L.d8[1][p * ms8:(p + 1) * ms8].clone() for p in range(8)]
+    tables = zq.gather_tables(gp_sl, gs_sl)
+    go = (torch.empty(mb8, dtype=torch.uint8, device="cuda"), torch.empty(ms8, dtype=torch.float32, device="cuda"))
+    gather_call = lambda: zq.qgz_reduce_level_gather(gp_sl, gs_sl, L.m8, GBLOCK, packed_out=go[0], scales_out=go[1],
+                                                     tables=tables)
+    contig_call = lambda: zq.qgz_reduce_level(L.d8[0], L.d8[1], 8, L.m8, GBLOCK, packed_out=L.o8[0],
+                                              scales_out=L.o8[1])
+    gtimes = {}
+    for name, fn in (("contiguous", contig_call), ("gather", gather_call)):
+        for _ in range(3):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        gtimes[name] = e0.elapsed_time(e1) * 1e3 / args.steps
+    same = bool(torch.equal(go[0], L.o8[0]) and torch.equal(go[1], L.o8[1]))
+    gather = {"P=8 level contiguous us": round(gtimes["contiguous"], 2), "P=8 level gather us": round(gtimes["gather"], 2),
+              "gather_GBps": round(bytes_reduce(8, L.m8, GBLOCK) / (gtimes["gather"] * 1e-6) / 1e9, 1),
+              "bit_identical": same}
+    del gp_sl, gs_sl, tables, go
+
     # next row: the degree-2 weight partition (1/2 shard quantised into its slot
     # of the gathered buffer; the dequantisation of the gathered layer is the
     # same call as in the step)
@@ -618,6 +648,7 @@ def main():
         "fused_last_level": fused,
         "sec_degree_2": sec_degree_2,
         "all_shares": all_shares,
+        "reduce_gather": gather,
         "dequant_gemm": dq_gemm,
         "copy_ceiling_GBps": round(copy_gbps, 1),
     }
