@@ -289,7 +289,7 @@ def check_against_oracle(L, outs):
 
 
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2501_04266_amd", "csrc", f)
-                  for f in ("zq_kernels.hip", "zq_internal.h", "zq_api.hip")]
+                  for f in ("zq_kernels.hip", "zq_internal.h", "zq_device.h", "zq_host.h", "zq_api.hip")]
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_pmc_traffic.txt")
 VALU_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_pmc_valu.txt")
 

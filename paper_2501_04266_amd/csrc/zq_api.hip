@@ -8,72 +8,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include <tuple>
-#include <utility>
-
 #include "zq.h"
+#include "zq_host.h"
 #include "zq_internal.h"
 
 namespace {
 
 using namespace zq;
-
-constexpr int64_t kMaxGrid = 0x7fffffff;  // workgroups per launch
-
-// Workgroups to cover `units` at `units_per_wg` each (0 if it exceeds the
-// launch limit; callers turn that into ZQ_E_SIZE before anything is enqueued).
-int64_t grid_for(int64_t units, int64_t units_per_wg) {
-  int64_t g = (units + units_per_wg - 1) / units_per_wg;
-  if (g < 1) g = 1;
-  return g > kMaxGrid ? 0 : g;
-}
-
-// Launch with the kernel's exact parameter types; returns ZQ_E_HIP when the
-// runtime rejects the launch.
-template <typename... KArgs, typename... Args>
-int launch(void (*kern)(KArgs...), unsigned grid, unsigned block, hipStream_t st, Args&&... args) {
-  std::tuple<KArgs...> tup(std::forward<Args>(args)...);
-  void* argv[sizeof...(KArgs)];
-  std::apply([&](auto&... a) {
-    int i = 0;
-    ((argv[i++] = static_cast<void*>(&a)), ...);
-  }, tup);
-  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(kern), dim3(grid), dim3(block), argv, 0, st);
-  return e == hipSuccess ? ZQ_OK : ZQ_E_HIP;
-}
-
-int log2_block(int32_t block) {
-  if (block < 32 || block > 1024 || (block & (block - 1)) != 0) return -1;
-  int lg = 0;
-  while ((1 << lg) < block) ++lg;
-  return lg;
-}
-
-bool dtype_ok(int dt) { return dt == ZQ_F32 || dt == ZQ_F16 || dt == ZQ_BF16; }
-int64_t elem_bytes(int dt) { return dt == ZQ_F32 ? 4 : 2; }
-bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
-
-struct Range {
-  const void* p;
-  int64_t bytes;
-};
-bool overlap(Range a, Range b) {
-  uintptr_t a0 = reinterpret_cast<uintptr_t>(a.p), b0 = reinterpret_cast<uintptr_t>(b.p);
-  return a0 < b0 + (uintptr_t)b.bytes && b0 < a0 + (uintptr_t)a.bytes;
-}
-bool any_overlap(std::initializer_list<Range> outs, std::initializer_list<Range> ins) {
-  for (const Range& o : outs) {
-    for (const Range& i : ins)
-      if (overlap(o, i)) return true;
-  }
-  // outputs must not overlap each other either
-  for (auto o1 = outs.begin(); o1 != outs.end(); ++o1)
-    for (auto o2 = o1 + 1; o2 != outs.end(); ++o2)
-      if (overlap(*o1, *o2)) return true;
-  return false;
-}
-
-int64_t num_scales(int64_t n, int32_t block) { return (n + block - 1) / block; }
 
 // Shared body of qwz_quantize / qgz_quantize.
 int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, float* scales, void* stream,
@@ -240,45 +181,6 @@ int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* co
                             int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream) {
   return reduce(reinterpret_cast<const uint8_t*>(packed_slices), reinterpret_cast<const float*>(scale_slices), P, m,
                 block, packed_out, scales_out, false, nullptr, -1, stream, true);
-}
-
-int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,
-                     int64_t K, int32_t block, float* y, void* stream) {
-  if (M < 0 || N < 0 || K < 0) return ZQ_E_SIZE;
-  const int lgB = log2_block(block);
-  if (lgB < 0) return ZQ_E_BLOCK;
-  if (xt != ZQ_BF16 && xt != ZQ_F16) return ZQ_E_DTYPE;
-  if (K % kDqGemmK != 0) return ZQ_E_SIZE;
-  if (M == 0 || N == 0) return ZQ_OK;
-  if (!y || (K > 0 && (!x || !codes || !scales))) return ZQ_E_NULL;
-  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, 4)) return ZQ_E_ALIGN;
-  if (any_overlap({{y, 4 * M * N}}, {{x, 2 * M * K}, {codes, N * K}, {scales, 4 * num_scales(N * K, block)}}))
-    return ZQ_E_ALIAS;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  const uint16_t* xh = static_cast<const uint16_t*>(x);
-  if (M > ZQ_GEMM_SMALL_M) {
-    const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
-    if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
-    return launch(dqgemm_kernel(xt, false, false), (unsigned)(mtiles * ntiles), kDqGemmThreads, st, xh, codes,
-                  scales, M, N, K, lgB, y, mtiles, ntiles, 1);
-  }
-  // few rows: small tiles, and K split across workgroups (partial tiles added
-  // into a zeroed y) when the tiles alone cannot fill the GPU
-  const int64_t mtiles = (M + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
-  const int64_t ntiles = (N + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
-  const int64_t tiles = mtiles * ntiles, ksteps = K / kDqGemmK;
-  int64_t splits = (kDqGemmSplitTarget + tiles - 1) / tiles;
-  if (splits > ksteps) splits = ksteps;
-  if (splits < 1) splits = 1;
-  if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
-  if (splits == 1)
-    return launch(dqgemm_kernel(xt, true, false), (unsigned)tiles, kDqGemmSmallThreads, st, xh, codes, scales, M, N,
-                  K, lgB, y, mtiles, ntiles, 1);
-  const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
-  int rc = launch(fill_zero_kernel(), (unsigned)fill_grid, 256u, st, y, count);
-  if (rc != ZQ_OK) return rc;
-  return launch(dqgemm_kernel(xt, true, true), (unsigned)(tiles * splits), kDqGemmSmallThreads, st, xh, codes,
-                scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
 }
 
 int64_t zq_num_scales(int64_t n, int32_t block) {

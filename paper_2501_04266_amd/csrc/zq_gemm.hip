@@ -32,11 +32,50 @@
 
 #include "zq.h"
 #include "zq_device.h"
-#include "zq_internal.h"
+#include "zq_host.h"
 
 #pragma clang fp contract(off)
 
 namespace zq {
+
+// dequantise-on-load GEMM (x of type xt = ZQ_BF16 or ZQ_F16)
+#ifndef ZQ_GEMM_BM
+#define ZQ_GEMM_BM 256
+#endif
+#ifndef ZQ_GEMM_BN
+#define ZQ_GEMM_BN 256
+#endif
+#ifndef ZQ_GEMM_WM
+#define ZQ_GEMM_WM 2
+#endif
+#ifndef ZQ_GEMM_WN
+#define ZQ_GEMM_WN 4
+#endif
+#ifndef ZQ_GEMM_RSETS
+#define ZQ_GEMM_RSETS 2
+#endif
+#ifndef ZQ_GEMM_PINGPONG
+#define ZQ_GEMM_PINGPONG 1
+#endif
+constexpr int kDqGemmTileM = ZQ_GEMM_BM;  // rows of y per workgroup
+constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
+constexpr int kDqGemmK = 64;              // K must be a multiple of this
+constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
+constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 22;  // 32-bit lane offsets in the ping-pong kernel
+// few rows (M <= this): 64 x 64 tiles over 4 waves, K split across
+// workgroups when the tiles alone cannot fill the GPU
+#ifndef ZQ_GEMM_SMALL_M
+#define ZQ_GEMM_SMALL_M 512
+#endif
+#ifndef ZQ_GEMM_SPLIT_TARGET
+#define ZQ_GEMM_SPLIT_TARGET 2048
+#endif
+constexpr int kDqGemmSmallTile = 64;
+constexpr int kDqGemmSmallThreads = 256;
+constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // workgroups a split launch aims for
+using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
+                              int64_t, int64_t, int);
+
 namespace {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -255,16 +294,213 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
     }
 }
 
+// The 256 x 256 tile with a ping-pong schedule (8 waves, two per SIMD).  Waves
+// w and w + 4 share a SIMD (a workgroup's waves are dealt to the 4 SIMDs round
+// robin) and run half a K-step (32 of K) out of phase: while one issues the 16
+// MFMAs of its half, the other reads its next operand fragments from LDS,
+// dequantises and stores its part of the next tile and issues its next global
+// loads, so the matrix core of each SIMD stays fed.  Each phase ends in a
+// workgroup barrier, which also orders the LDS traffic: tile kt + 1 is written
+// during the four phases of K-step kt (two per wave group) into the buffer
+// that tile kt - 1 occupied, whose last reads completed before the preceding
+// barrier, and is first read in the phase after the last of them.  Sums run in
+// the same order as in k_dqgemm, so the two give identical bits.
+__device__ __forceinline__ void phase_end() {
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+template <int XT>
+__global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+                                                  const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
+                                                  int lgB, float* __restrict__ y, int64_t mtiles, int64_t ntiles,
+                                                  int /*splits*/) {
+  constexpr int BM = 256, BN = 256, WN = 4, NT = 512;
+  constexpr int TI = 4, TJ = 2;                  // 32 x 32 MFMA tiles per wave (128 x 64)
+  constexpr int XC = BM * kBK / 8 / NT;          // 4 x chunks per thread and K-step
+  constexpr int WC = BN * kBK / 16 / NT;         // 2 code chunks per thread and K-step
+  static_assert(XC == 4 && WC == 2, "tile shape");
+  __shared__ u32x4 As[2][BM * kLDK / 8];
+  __shared__ u32x4 Bs[2][BN * kLDK / 8];
+
+  const int64_t T = mtiles * ntiles;
+  const int64_t wg = blockIdx.x;
+  const int64_t q = T / kXcds, r = T % kXcds, xcd = wg % kXcds, idx = wg / kXcds;
+  const int64_t t = !ZQ_GEMM_XCD_MAP ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int64_t per_group = (int64_t)kGroupM * ntiles;
+  const int64_t first_m = (t / per_group) * kGroupM;
+  const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
+  const int64_t mt = first_m + (t % per_group) % gsize;
+  const int64_t nt = (t % per_group) / gsize;
+  const int64_t m0 = mt * BM, n0 = nt * BN;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
+  const int KT = (int)(K / kBK);
+
+  // tile kt + 1 is held in registers from its loads (phases of K-step kt - 1)
+  // to its LDS store (phases of K-step kt): part P of a tile is x chunks 2P,
+  // 2P + 1 and code chunk P of each thread, stored and then reloaded with the
+  // next tile's part in the same phase, which leaves each load a whole K-step
+  // (four phases) to arrive
+  u32x4 xrs[1][XC], wrs[1][WC];
+  float srs[1][WC];
+  // Loads address the tile through wave-uniform bases (scalar registers) and
+  // loop-invariant 32-bit lane offsets (the host keeps K <= kDqGemmPpMaxK so
+  // that 512 K bytes fit).  Rows past M (columns past N) of a ragged edge
+  // tile read row M - 1 (N - 1) instead: they only enter outputs that are
+  // never stored, and unconditional loads keep the wait counts exact.  The
+  // scale base is exact because n0 K is a multiple of 256 * 64 >= B.
+  uint32_t xoff[XC], woff[WC];
+#pragma unroll
+  for (int i = 0; i < XC; ++i) {
+    const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
+    const int64_t m = m0 + row < M ? m0 + row : M - 1;
+    xoff[i] = (uint32_t)(((m - m0) * K + col) * 2);
+  }
+#pragma unroll
+  for (int i = 0; i < WC; ++i) {
+    const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
+    const int64_t n = n0 + row < N ? n0 + row : N - 1;
+    woff[i] = (uint32_t)((n - n0) * K + col);
+  }
+  const char* xbase = reinterpret_cast<const char*>(x + m0 * K);
+  const int8_t* wbase = codes + n0 * K;
+  const float* sbase = scales + ((n0 * K) >> lgB);
+  auto gload = [&](int kt, auto part_c) {
+    constexpr int R = 0, P = decltype(part_c)::value;
+    const uint32_t k0 = (uint32_t)kt * kBK;
+    const char* xk = xbase + 2 * (int64_t)k0;
+    const int8_t* wk = wbase + k0;
+#pragma unroll
+    for (int i = 2 * P; i < 2 * P + 2; ++i) xrs[R][i] = *reinterpret_cast<const u32x4*>(xk + xoff[i]);
+    wrs[R][P] = *reinterpret_cast<const u32x4*>(wk + woff[P]);
+    srs[R][P] = sbase[(woff[P] + k0) >> lgB];
+  };
+  auto sstore = [&](int buf, auto part_c) {
+    constexpr int R = 0, P = decltype(part_c)::value;
+#pragma unroll
+    for (int i = 2 * P; i < 2 * P + 2; ++i) {
+      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
+      As[buf][(row * kLDK + col) / 8] = xrs[R][i];
+    }
+    {
+      const int i = P;
+      const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
+      uint32_t o[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t word = wrs[R][i][j >> 1];
+        const int sh = (j & 1) * 16;
+        const float v0 = (float)(int32_t)(int8_t)(word >> sh) * srs[R][i];
+        const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * srs[R][i];
+        o[j] = narrow2<XT>(v0, v1);
+      }
+      Bs[buf][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
+      Bs[buf][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
+    }
+  };
+
+  f32x16_t acc[TI][TJ];
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+
+  // operand fragments of one half K-step: k steps 2H and 2H + 1 of 16
+  const int frow = lane & 31, fk = 8 * (lane >> 5);
+  u32x4 fa[TI][2], fb[TJ][2];
+  auto read_frags = [&](int buf, auto half_c) {
+    constexpr int H = decltype(half_c)::value;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int kk = 2 * H + s;
+#pragma unroll
+      for (int i = 0; i < TI; ++i) fa[i][s] = As[buf][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+#pragma unroll
+      for (int j = 0; j < TJ; ++j) fb[j][s] = Bs[buf][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+    }
+  };
+  auto mma = [&]() {
+    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32<XT>(fa[i][s], fb[j][s], acc[i][j]);
+    __builtin_amdgcn_s_setprio(0);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  // K-step kt from LDS buffer kt % 2; with ST, tile kt + 1 goes from the
+  // registers into the other buffer, and with LD tile kt + 2 is then loaded
+  // into the registers.  The steady-state loop has both and no branches, so
+  // each phase waits only for the loads of the part it stores.
+  auto kstep = [&](int kt, auto st_c, auto ld_c) {
+    constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
+    const int cur = kt & 1;
+    read_frags(cur, I0{});
+    if constexpr (ST) sstore(cur ^ 1, I0{});
+    if constexpr (LD) gload(kt + 2, I0{});
+    phase_end();
+    mma();
+    phase_end();
+    read_frags(cur, I1{});
+    if constexpr (ST) sstore(cur ^ 1, I1{});
+    if constexpr (LD) gload(kt + 2, I1{});
+    phase_end();
+    mma();
+    phase_end();
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
+
+  if (KT > 0) {
+    gload(0, I0{});
+    gload(0, I1{});
+    sstore(0, I0{});
+    sstore(0, I1{});
+  }
+  if (KT > 1) {
+    gload(1, I0{});
+    gload(1, I1{});
+  }
+  __syncthreads();
+  if (wm == 1) phase_end();  // the second wave group starts one phase later
+  int kt = 0;
+#pragma unroll 1
+  for (; kt + 2 < KT; ++kt) kstep(kt, T_{}, T_{});
+  if (kt + 1 < KT) kstep(kt++, T_{}, F_{});
+  if (kt < KT) kstep(kt, F_{}, F_{});
+  if (wm == 0) phase_end();  // ... and the first one waits for its last phase
+
+#pragma unroll
+  for (int i = 0; i < TI; ++i)
+#pragma unroll
+    for (int j = 0; j < TJ; ++j) {
+      const int64_t n = n0 + wn * TJ * 32 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t m = m0 + wm * TI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (m < M && n < N) y[m * N + n] = acc[i][j][e];
+      }
+    }
+}
+
 // y[0, count) = 0 (for the split kernel, which adds into y)
 __global__ void __launch_bounds__(256) k_fill_zero(float* __restrict__ y, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) y[i] = 0.0f;
 }
 
-}  // namespace
-
+static_assert(!ZQ_GEMM_PINGPONG || (kDqGemmTileM == 256 && kDqGemmTileN == 256 && kDqGemmThreads == 512), "ping-pong tile");
 static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads && 64 * 2 * 2 == kDqGemmSmallThreads, "launch shape");
 
-DqGemmKernel dqgemm_kernel(int xt, bool small, bool split) {
+// pp: the large tile's ping-pong kernel, for K <= kDqGemmPpMaxK
+DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
+  if (!small && ZQ_GEMM_PINGPONG && pp) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16> : &k_dqgemm_pp<ZQ_F16>;
   if (!small)
     return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
                          : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
@@ -275,6 +511,48 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split) {
                        : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false>;
 }
 
-FillZeroKernel fill_zero_kernel() { return &k_fill_zero; }
-
+}  // namespace
 }  // namespace zq
+
+using namespace zq;
+
+// qwz_dequant_gemm (include/zq.h): argument checks, then one launch (or a
+// zero fill and a split-K launch for few rows)
+int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,
+                     int64_t K, int32_t block, float* y, void* stream) {
+  if (M < 0 || N < 0 || K < 0) return ZQ_E_SIZE;
+  const int lgB = log2_block(block);
+  if (lgB < 0) return ZQ_E_BLOCK;
+  if (xt != ZQ_BF16 && xt != ZQ_F16) return ZQ_E_DTYPE;
+  if (K % kDqGemmK != 0) return ZQ_E_SIZE;
+  if (M == 0 || N == 0) return ZQ_OK;
+  if (!y || (K > 0 && (!x || !codes || !scales))) return ZQ_E_NULL;
+  if (!aligned(x, 16) || !aligned(codes, 16) || !aligned(scales, 4) || !aligned(y, 4)) return ZQ_E_ALIGN;
+  if (any_overlap({{y, 4 * M * N}}, {{x, 2 * M * K}, {codes, N * K}, {scales, 4 * num_scales(N * K, block)}}))
+    return ZQ_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const uint16_t* xh = static_cast<const uint16_t*>(x);
+  if (M > ZQ_GEMM_SMALL_M) {
+    const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
+    if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
+    return launch(dqgemm_kernel(xt, false, false, K <= kDqGemmPpMaxK), (unsigned)(mtiles * ntiles), kDqGemmThreads,
+                  st, xh, codes, scales, M, N, K, lgB, y, mtiles, ntiles, 1);
+  }
+  // few rows: small tiles, and K split across workgroups (partial tiles added
+  // into a zeroed y) when the tiles alone cannot fill the GPU
+  const int64_t mtiles = (M + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
+  const int64_t ntiles = (N + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
+  const int64_t tiles = mtiles * ntiles, ksteps = K / kDqGemmK;
+  int64_t splits = (kDqGemmSplitTarget + tiles - 1) / tiles;
+  if (splits > ksteps) splits = ksteps;
+  if (splits < 1) splits = 1;
+  if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
+  if (splits == 1)
+    return launch(dqgemm_kernel(xt, true, false, false), (unsigned)tiles, kDqGemmSmallThreads, st, xh, codes, scales,
+                  M, N, K, lgB, y, mtiles, ntiles, 1);
+  const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
+  int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
+  if (rc != ZQ_OK) return rc;
+  return launch(dqgemm_kernel(xt, true, true, false), (unsigned)(tiles * splits), kDqGemmSmallThreads, st, xh, codes,
+                scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
+}

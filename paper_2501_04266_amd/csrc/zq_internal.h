@@ -94,41 +94,4 @@ ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
 ReduceKernel reduce_gather_kernel(int lgB, ReduceShape shape);
 ReduceGenericKernel reduce_generic_kernel(bool gather);
 
-// dequantise-on-load GEMM (x of type xt = ZQ_BF16 or ZQ_F16)
-#ifndef ZQ_GEMM_BM
-#define ZQ_GEMM_BM 256
-#endif
-#ifndef ZQ_GEMM_BN
-#define ZQ_GEMM_BN 256
-#endif
-#ifndef ZQ_GEMM_WM
-#define ZQ_GEMM_WM 2
-#endif
-#ifndef ZQ_GEMM_WN
-#define ZQ_GEMM_WN 4
-#endif
-#ifndef ZQ_GEMM_RSETS
-#define ZQ_GEMM_RSETS 2
-#endif
-constexpr int kDqGemmTileM = ZQ_GEMM_BM;  // rows of y per workgroup
-constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
-constexpr int kDqGemmK = 64;              // K must be a multiple of this
-constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
-// few rows (M <= this): 64 x 64 tiles over 4 waves, K split across
-// workgroups when the tiles alone cannot fill the GPU
-#ifndef ZQ_GEMM_SMALL_M
-#define ZQ_GEMM_SMALL_M 512
-#endif
-#ifndef ZQ_GEMM_SPLIT_TARGET
-#define ZQ_GEMM_SPLIT_TARGET 2048
-#endif
-constexpr int kDqGemmSmallTile = 64;
-constexpr int kDqGemmSmallThreads = 256;
-constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // workgroups a split launch aims for
-using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
-                              int64_t, int64_t, int);
-using FillZeroKernel = void (*)(float*, int64_t);
-DqGemmKernel dqgemm_kernel(int xt, bool small, bool split);
-FillZeroKernel fill_zero_kernel();
-
 }  // namespace zq

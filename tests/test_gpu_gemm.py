@@ -36,8 +36,11 @@ def _exact_inputs(M, N, K, B, dtype, seed):
     return x, codes, scales
 
 
+# M <= 512: the few-row path; M > 512: the 256 x 256 tile path, with ragged
+# edges in M and N and 1, 2, 3 and 10 K-steps of 64
 EXACT = [(1, 1, 64, 256), (37, 100, 192, 32), (128, 128, 64, 256), (300, 257, 1024, 128), (129, 383, 640, 64),
-         (256, 512, 6144, 256)]
+         (256, 512, 6144, 256), (600, 300, 64, 256), (513, 257, 128, 64), (777, 520, 192, 32),
+         (1024, 512, 640, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
