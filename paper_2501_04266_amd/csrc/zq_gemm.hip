@@ -61,7 +61,7 @@ constexpr int kDqGemmTileM = ZQ_GEMM_BM;  // rows of y per workgroup
 constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
 constexpr int kDqGemmK = 64;              // K must be a multiple of this
 constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
-constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 22;  // 32-bit lane offsets in the ping-pong kernel
+constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 21;  // 32-bit buffer offsets in the ping-pong kernel
 // few rows (M <= this): 64 x 64 tiles over 4 waves, K split across
 // workgroups when the tiles alone cannot fill the GPU
 #ifndef ZQ_GEMM_SMALL_M
@@ -83,7 +83,10 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
 
 constexpr int kBK = 64;
+// buffer resource word 3 for raw (untyped) buffer loads on gfx9-family targets
+constexpr int kBufferFlags = 0x00020000;
 constexpr int kLDK = kBK + 8;  // LDS row stride in 16-bit elements (144 bytes)
+constexpr int kRow16 = kLDK / 8;  // the same in 16-byte units
 #ifndef ZQ_GEMM_GROUP_M
 #define ZQ_GEMM_GROUP_M 4
 #endif
@@ -345,60 +348,67 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
   // (four phases) to arrive
   u32x4 xrs[1][XC], wrs[1][WC];
   float srs[1][WC];
-  // Loads address the tile through wave-uniform bases (scalar registers) and
-  // loop-invariant 32-bit lane offsets (the host keeps K <= kDqGemmPpMaxK so
-  // that 512 K bytes fit).  Rows past M (columns past N) of a ragged edge
-  // tile read row M - 1 (N - 1) instead: they only enter outputs that are
-  // never stored, and unconditional loads keep the wait counts exact.  The
-  // scale base is exact because n0 K is a multiple of 256 * 64 >= B.
+  // Loads are buffer loads: a wave-uniform resource per operand (base at the
+  // tile's first row, size up to the operand's last row in the tile) plus
+  // loop-invariant 32-bit lane offsets (the host keeps K <= kDqGemmPpMaxK, so
+  // 256 rows of 2 K bytes fit) and the K-step's byte offset in a scalar
+  // register.  Rows past M (columns past N) of a ragged edge tile fall
+  // outside the resource and read as zero; they only enter outputs that are
+  // never stored.  The scales' base index n0 K / B is exact because n0 K is a
+  // multiple of 256 * 64 >= B.
   uint32_t xoff[XC], woff[WC];
 #pragma unroll
   for (int i = 0; i < XC; ++i) {
     const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-    const int64_t m = m0 + row < M ? m0 + row : M - 1;
-    xoff[i] = (uint32_t)(((m - m0) * K + col) * 2);
+    xoff[i] = (uint32_t)((row * K + col) * 2);
   }
 #pragma unroll
   for (int i = 0; i < WC; ++i) {
     const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
-    const int64_t n = n0 + row < N ? n0 + row : N - 1;
-    woff[i] = (uint32_t)((n - n0) * K + col);
+    woff[i] = (uint32_t)(row * K + col);
   }
-  const char* xbase = reinterpret_cast<const char*>(x + m0 * K);
-  const int8_t* wbase = codes + n0 * K;
-  const float* sbase = scales + ((n0 * K) >> lgB);
+  const int64_t mrows = M - m0 < BM ? M - m0 : BM, nrows = N - n0 < BN ? N - n0 : BN;
+  const __amdgpu_buffer_rsrc_t xres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(x + m0 * K), (short)0, (int)(mrows * K * 2), kBufferFlags);
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(codes + n0 * K), (short)0, (int)(nrows * K), kBufferFlags);
+  const int64_t s0 = (n0 * K) >> lgB, s1 = ((n0 + nrows) * K + (1 << lgB) - 1) >> lgB;
+  const __amdgpu_buffer_rsrc_t sres =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(scales + s0), (short)0, (int)((s1 - s0) * 4), kBufferFlags);
   auto gload = [&](int kt, auto part_c) {
     constexpr int R = 0, P = decltype(part_c)::value;
-    const uint32_t k0 = (uint32_t)kt * kBK;
-    const char* xk = xbase + 2 * (int64_t)k0;
-    const int8_t* wk = wbase + k0;
+    const int k0 = kt * kBK;
 #pragma unroll
-    for (int i = 2 * P; i < 2 * P + 2; ++i) xrs[R][i] = *reinterpret_cast<const u32x4*>(xk + xoff[i]);
-    wrs[R][P] = *reinterpret_cast<const u32x4*>(wk + woff[P]);
-    srs[R][P] = sbase[(woff[P] + k0) >> lgB];
+    for (int i = 2 * P; i < 2 * P + 2; ++i)
+      xrs[R][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xres, (int)xoff[i], 2 * k0, 0));
+    wrs[R][P] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, (int)woff[P], k0, 0));
+    const uint32_t si = (woff[P] + (uint32_t)k0) >> lgB;
+    srs[R][P] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(sres, (int)(si * 4), 0, 0));
   };
-  auto sstore = [&](int buf, auto part_c) {
-    constexpr int R = 0, P = decltype(part_c)::value;
+  // part P of the register tile: its 16 codes become fl(q * s) narrowed to
+  // XT in ob (deq), then x's chunks and ob go to LDS buffer `buf` (store)
+  uint32_t ob[8];
+  auto deq = [&](auto part_c) {
+    constexpr int P = decltype(part_c)::value;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint32_t word = wrs[0][P][j >> 1];
+      const int sh = (j & 1) * 16;
+      const float v0 = (float)(int32_t)(int8_t)(word >> sh) * srs[0][P];
+      const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * srs[0][P];
+      ob[j] = narrow2<XT>(v0, v1);
+    }
+  };
+  auto store = [&](int buf, auto part_c) {
+    constexpr int P = decltype(part_c)::value;
 #pragma unroll
     for (int i = 2 * P; i < 2 * P + 2; ++i) {
-      const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      As[buf][(row * kLDK + col) / 8] = xrs[R][i];
+      const int c = tid + NT * i;
+      As[buf][(c >> 3) * kRow16 + (c & 7)] = xrs[0][i];
     }
-    {
-      const int i = P;
-      const int c = tid + NT * i, row = c >> 2, col = (c & 3) * 16;
-      uint32_t o[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const uint32_t word = wrs[R][i][j >> 1];
-        const int sh = (j & 1) * 16;
-        const float v0 = (float)(int32_t)(int8_t)(word >> sh) * srs[R][i];
-        const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * srs[R][i];
-        o[j] = narrow2<XT>(v0, v1);
-      }
-      Bs[buf][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
-      Bs[buf][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
-    }
+    const int c = tid + NT * P, bi = (c >> 2) * kRow16 + (c & 3) * 2;
+    Bs[buf][bi] = u32x4{ob[0], ob[1], ob[2], ob[3]};
+    Bs[buf][bi + 1] = u32x4{ob[4], ob[5], ob[6], ob[7]};
   };
 
   f32x16_t acc[TI][TJ];
@@ -410,7 +420,10 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
   // operand fragments of one half K-step: k steps 2H and 2H + 1 of 16
-  const int frow = lane & 31, fk = 8 * (lane >> 5);
+  // (LDS indices in 16-byte units: a row is kRow16 of them, so the
+  // per-fragment offsets are constants)
+  const int frow = lane & 31;
+  const int abase = (wm * TI * 32 + frow) * kRow16 + (lane >> 5), bbase = (wn * TJ * 32 + frow) * kRow16 + (lane >> 5);
   u32x4 fa[TI][2], fb[TJ][2];
   auto read_frags = [&](int buf, auto half_c) {
     constexpr int H = decltype(half_c)::value;
@@ -418,12 +431,17 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
     for (int s = 0; s < 2; ++s) {
       const int kk = 2 * H + s;
 #pragma unroll
-      for (int i = 0; i < TI; ++i) fa[i][s] = As[buf][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int i = 0; i < TI; ++i) fa[i][s] = As[buf][abase + i * 32 * kRow16 + kk * 2];
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) fb[j][s] = Bs[buf][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int j = 0; j < TJ; ++j) fb[j][s] = Bs[buf][bbase + j * 32 * kRow16 + kk * 2];
     }
   };
-  auto mma = [&]() {
+  // the 16 MFMAs of a half K-step; with DQ, the dequantisation of code part
+  // P is interleaved with them (the matrix core runs each MFMA for 32 cycles,
+  // in which this wave's own VALU is otherwise idle)
+  auto mma = [&](auto part_c, auto dq_c) {
+    constexpr int P = decltype(part_c)::value;
+    constexpr bool DQ = decltype(dq_c)::value;
     __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int s = 0; s < 2; ++s)
@@ -431,28 +449,42 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32<XT>(fa[i][s], fb[j][s], acc[i][j]);
+    if constexpr (DQ) {
+      deq(part_c);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // 4 MFMAs first: the codes may still be arriving
+#pragma unroll
+      for (int q = 0; q < 10; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // 4 VALU
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    }
+    (void)P;
     __builtin_amdgcn_s_setprio(0);
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
-  // K-step kt from LDS buffer kt % 2; with ST, tile kt + 1 goes from the
-  // registers into the other buffer, and with LD tile kt + 2 is then loaded
-  // into the registers.  The steady-state loop has both and no branches, so
-  // each phase waits only for the loads of the part it stores.
+  // K-step kt from LDS buffer kt % 2.  With ST, tile kt + 1 goes from the
+  // registers into the other buffer (part 0 in the first phase, part 1 in the
+  // second; each B part was dequantised during the preceding MFMA phase), and
+  // with LD tile kt + 2 is loaded into the registers (part P right after part
+  // P of tile kt + 1 left them) and its part 0 dequantised.  The steady-state
+  // loop has both and no branches, so each wait covers exactly the loads it
+  // needs.
   auto kstep = [&](int kt, auto st_c, auto ld_c) {
     constexpr bool ST = decltype(st_c)::value, LD = decltype(ld_c)::value;
     const int cur = kt & 1;
+    if constexpr (ST) store(cur ^ 1, I0{});
     read_frags(cur, I0{});
-    if constexpr (ST) sstore(cur ^ 1, I0{});
     if constexpr (LD) gload(kt + 2, I0{});
     phase_end();
-    mma();
+    mma(I1{}, st_c);
     phase_end();
+    if constexpr (ST) store(cur ^ 1, I1{});
     read_frags(cur, I1{});
-    if constexpr (ST) sstore(cur ^ 1, I1{});
     if constexpr (LD) gload(kt + 2, I1{});
     phase_end();
-    mma();
+    mma(I0{}, ld_c);
     phase_end();
   };
   using T_ = std::true_type;
@@ -461,12 +493,21 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
   if (KT > 0) {
     gload(0, I0{});
     gload(0, I1{});
-    sstore(0, I0{});
-    sstore(0, I1{});
+    deq(I0{});
+    store(0, I0{});
+    deq(I1{});
+    store(0, I1{});
   }
+  // the loads of tile 1 in the loop's order (part 0, then part 1), so that
+  // the wait counts at the loop head are those of the steady state; its
+  // part 0 is dequantised here, as the loop does for the tiles after it
   if (KT > 1) {
+    __builtin_amdgcn_sched_barrier(0);
     gload(1, I0{});
+    __builtin_amdgcn_sched_barrier(0);
     gload(1, I1{});
+    __builtin_amdgcn_sched_barrier(0);
+    deq(I0{});
   }
   __syncthreads();
   if (wm == 1) phase_end();  // the second wave group starts one phase later
