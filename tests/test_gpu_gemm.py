@@ -129,6 +129,33 @@ def test_gpt20b_layer_gemms_sampled_rows():
         off += N * K
 
 
+@pytest.mark.parametrize("K", [1 << 21, (1 << 21) + 256])
+def test_dequant_gemm_long_k(K):
+    """Reductions as long as 2^21 take the ping-pong schedule (32-bit lane
+    offsets); longer ones the plain 256 x 256 schedule (64-bit addresses).
+    x is zero outside two 4096-column windows at the start and the end of K,
+    so the result equals the oracle's GEMM over those columns alone (zero
+    terms add exactly); x = a/4 with |a| <= 8 and scales 2^-7 keep every
+    partial sum a multiple of 2^-9 below 2^14, exact in binary32."""
+    M, N, B, W = 513, 3, 256, 4096
+    rng = np.random.default_rng(K % 1000)
+    xs = wl.to_storage((rng.integers(-8, 9, (M, 2 * W)) / 4.0).astype(np.float32).reshape(-1), "bf16").reshape(M, 2 * W)
+    codes = rng.integers(-127, 128, N * K).astype(np.int8)
+    scales = np.full(N * K // B, 2.0 ** -7, np.float32)
+    xd = torch.zeros((M, K), dtype=torch.bfloat16, device="cuda")
+    xd[:, :W] = to_dev(np.ascontiguousarray(xs[:, :W]), "bf16")
+    xd[:, K - W:] = to_dev(np.ascontiguousarray(xs[:, W:]), "bf16")
+    y = zq.qwz_dequant_gemm(xd, to_dev(codes), to_dev(scales), N, B)
+    torch.cuda.synchronize()
+    cw = codes.reshape(N, K)
+    sub_codes = np.ascontiguousarray(np.concatenate([cw[:, :W], cw[:, K - W:]], axis=1)).reshape(-1)
+    sub_scales = np.full(N * 2 * W // B, 2.0 ** -7, np.float32)
+    want = oracle.qwz_dequant_gemm(xs, sub_codes, sub_scales, N, B, "bf16")
+    got = from_dev(y).astype(np.float64)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
+
+
 @pytest.mark.parametrize("M", [64, 640])
 def test_dequant_gemm_graph_capture(M):
     """The GEMM (both the few-row split path, which also launches its own
