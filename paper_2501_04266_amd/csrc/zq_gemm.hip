@@ -71,6 +71,10 @@ constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 21;  // 32-bit buffer offsets in
 #define ZQ_GEMM_SPLIT_TARGET 2048
 #endif
 constexpr int kDqGemmSmallTile = 64;
+#ifndef ZQ_GEMM_SMALL_RSETS
+#define ZQ_GEMM_SMALL_RSETS 3
+#endif
+constexpr int kDqGemmSmallRsets = ZQ_GEMM_SMALL_RSETS;  // register sets (K-steps of loads ahead) of the small tiles
 constexpr int kDqGemmSmallThreads = 256;
 constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // workgroups a split launch aims for
 using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
@@ -96,6 +100,15 @@ constexpr int kRow16 = kLDK / 8;  // the same in 16-byte units
 constexpr int kGroupM = ZQ_GEMM_GROUP_M;  // tile rows sharing a weight tile in L2
 constexpr int kXcds = 8;
 
+// f(integral_constant<int, i>) for i = I .. N - 1
+template <int I, int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (I < N) {
+    f(std::integral_constant<int, I>{});
+    static_for<I + 1, N>(f);
+  }
+}
+
 template <int XT>
 __device__ __forceinline__ f32x16_t mfma32(u32x4 a, u32x4 b, f32x16_t c) {
   if constexpr (XT == ZQ_BF16)
@@ -118,7 +131,7 @@ __device__ __forceinline__ uint32_t narrow2(float a, float b) {
 // SPLIT: workgroup w takes K-steps [s KT / splits, (s + 1) KT / splits) of
 // tile w / splits (s = w % splits) and adds its partial tile into y, which the
 // host has zeroed; used when there are too few tiles to fill the GPU.
-template <int XT, int BM, int BN, int WM, int WN, bool SPLIT>
+template <int XT, int BM, int BN, int WM, int WN, bool SPLIT, int RS = ZQ_GEMM_RSETS>
 __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                          const float* __restrict__ scales, int64_t M, int64_t N,
                                                          int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
@@ -151,9 +164,8 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
   const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
 
-  // RS register sets: with 2, tile t's loads are issued two K-steps before
-  // its LDS store
-  constexpr int RS = ZQ_GEMM_RSETS;
+  // RS register sets: tile t's loads are issued RS K-steps before its LDS
+  // store
   u32x4 xrs[RS][XC], wrs[RS][WC];
   float srs[RS][WC];
   // global -> registers: x rows m0.., 8 elements per chunk; codes rows n0..,
@@ -255,7 +267,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
       if (kt + 1 < KT) sstore(cur ^ 1, R0{});
       __syncthreads();
     }
-  } else {
+  } else if constexpr (RS == 2) {
     // tile t lives in register set t % 2 from its load (K-step t - 2) to its
     // store (end of K-step t - 1)
     if (KT > 0) {
@@ -278,6 +290,44 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
         __syncthreads();
       }
     }
+  } else {
+    // tile t lives in register set t % RS from its loads (K-step t - RS) to
+    // its store (end of K-step t - 1).  Buffer parity and set index repeat
+    // every 2 RS K-steps; the steady-state block has no branches, so each
+    // wait covers exactly the loads it needs.
+    constexpr int U = 2 * RS;
+    if (KT > 0) {
+      gload(0, R0{});
+      sstore(0, R0{});
+    }
+    static_for<1, RS + 1>([&](auto rc) {
+      constexpr int r = decltype(rc)::value;
+      if (r < KT) gload(r, std::integral_constant<int, r % RS>{});
+    });
+    __syncthreads();
+    int kt = 0;
+#pragma unroll 1
+    for (; kt + U + RS + 1 <= KT; kt += U) {
+      static_for<0, U>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        using S = std::integral_constant<int, (j + 1) % RS>;
+        compute(j & 1);
+        sstore((j + 1) & 1, S{});
+        gload(kt + j + 1 + RS, S{});
+        __syncthreads();
+      });
+    }
+    static_for<0, U + RS + 1>([&](auto jc) {
+      constexpr int j = decltype(jc)::value;
+      using S = std::integral_constant<int, (j + 1) % RS>;
+      const int t = kt + j;
+      if (t < KT) {
+        compute(j & 1);
+        if (t + 1 < KT) sstore((j + 1) & 1, S{});
+        if (t + 1 + RS < KT) gload(t + 1 + RS, S{});
+      }
+      __syncthreads();
+    });
   }
 
   // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32
@@ -545,10 +595,10 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
     return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
                          : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
   if (split)
-    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true>
-                         : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true>;
-  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false>
-                       : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false>;
+    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>
+                         : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>;
+  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>
+                       : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>;
 }
 
 }  // namespace
