@@ -252,22 +252,8 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   };
 
   using R0 = std::integral_constant<int, 0>;
-  using R1 = std::integral_constant<int, RS - 1>;
-  if constexpr (RS == 1) {
-    if (KT > 0) {
-      gload(0, R0{});
-      sstore(0, R0{});
-    }
-    __syncthreads();
-#pragma unroll 1
-    for (int kt = 0; kt < KT; ++kt) {
-      const int cur = kt & 1;
-      if (kt + 1 < KT) gload(kt + 1, R0{});
-      compute(cur);
-      if (kt + 1 < KT) sstore(cur ^ 1, R0{});
-      __syncthreads();
-    }
-  } else if constexpr (RS == 2) {
+  using R1 = std::integral_constant<int, 1>;
+  if constexpr (RS == 2) {
     // tile t lives in register set t % 2 from its load (K-step t - 2) to its
     // store (end of K-step t - 1)
     if (KT > 0) {
