@@ -14,17 +14,21 @@
 // binary32 and summed in binary32 by the MFMA units (v_mfma_f32_32x32x16_bf16
 // / _f16), in an order the hardware fixes.
 //
-// Tiling: a workgroup of 8 waves computes a 256 x 256 tile of y, each wave a
-// 128 x 64 block as 4 x 2 MFMA tiles of 32 x 32 (other shapes are template
-// parameters).  K advances 64 at a time.  x tiles (16 B per load) and code
-// tiles (16 codes and their scale per load) are fetched into one of two
-// register sets two K-steps ahead, so a load has a whole K-step of MFMAs to
-// arrive in; at the end of each K-step the next tile is dequantised and
-// stored into the LDS buffer not being read.  LDS rows are padded by 16 bytes so the 16-byte
-// fragment reads of 8 consecutive lanes fall in distinct banks.  Workgroups
-// are numbered so that each XCD receives a contiguous range of tiles, and
-// within it groups of 4 tile rows share their weight tiles through that XCD's
-// L2.
+// Kernels (all tile y with 32 x 32 MFMA tiles, K advancing 64 at a time,
+// LDS rows padded by 16 bytes so that the 16-byte fragment reads of 16
+// consecutive lanes fall in distinct banks):
+//   k_dqgemm_pp  many rows: 256 x 256 tiles over 8 waves (128 x 64 each) in a
+//                ping-pong schedule, waves w and w + 4 of a SIMD half a K-step
+//                apart (one stores the next tile and reads its fragments
+//                while the other runs its MFMAs, with its loads and
+//                dequantisation in between); buffer loads, none predicated.
+//   k_dqgemm     few rows: 64 x 64 tiles over 4 waves with RS register sets
+//                of loads in flight and K split across workgroups when the
+//                tiles alone are too few; also the many-row fallback for
+//                K > kDqGemmPpMaxK (256 x 256, two sets).
+// Many-row workgroups are numbered so that each XCD receives a contiguous
+// range of tiles, and within it groups of 4 tile rows share their weight
+// tiles through that XCD's L2.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -335,10 +339,11 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
 
 // The 256 x 256 tile with a ping-pong schedule (8 waves, two per SIMD).  Waves
 // w and w + 4 share a SIMD (a workgroup's waves are dealt to the 4 SIMDs round
-// robin) and run half a K-step (32 of K) out of phase: while one issues the 16
-// MFMAs of its half, the other reads its next operand fragments from LDS,
-// dequantises and stores its part of the next tile and issues its next global
-// loads, so the matrix core of each SIMD stays fed.  Each phase ends in a
+// robin) and run half a K-step (32 of K) out of phase: while one runs the 16
+// MFMAs of its half (with its next global loads and the dequantisation of its
+// next weight chunk interleaved), the other stores its part of the next tile
+// into LDS and reads its next operand fragments, so the matrix core of each
+// SIMD stays fed.  Each phase ends in a
 // workgroup barrier, which also orders the LDS traffic: tile kt + 1 is written
 // during the four phases of K-step kt (two per wave group) into the buffer
 // that tile kt - 1 occupied, whose last reads completed before the preceding
