@@ -146,15 +146,17 @@ N_EDGE = 123_456_789
 # 128 elements of an N(0, 1e-3) gradient is about [3e-4, 8e-4]
 ALL_SHARES_SCALES = (2e-4, 1e-3)
 
-CONFIGS = {
-    1: dict(name="tiny-1024x1024", n=N_TINY, wdtype="f16", wblock=256, shard=1, qwz_out="f16",
-            gblock=128, fanins=[2], gout="f32"),
-    2: dict(name="gpt-1.3b-layer", n=N_13B, wdtype="bf16", wblock=256, shard=8, qwz_out="bf16",
-            gblock=128, fanins=[8], gout="f32"),
-    3: dict(name="gpt-20b-layer", n=N_20B, wdtype="bf16", wblock=256, shard=8, qwz_out="bf16",
-            gblock=128, fanins=[8], gout="f32"),
-    4: dict(name="gpt-20b-3level", n=N_20B, wdtype=None, wblock=None, shard=None, qwz_out=None,
-            gblock=128, fanins=[2, 4, 48], gout="f32"),
-    5: dict(name="outlier-edge-123456789", n=N_EDGE, wdtype="f32", wblock=256, shard=1, qwz_out="bf16",
-            gblock=64, fanins=[], gout="bf16"),
+# the five workloads, by name: sizes, storage types, blocks, shard degree,
+# the weight dequantisation output, and the fan-ins of the gradient levels
+WORKLOADS = {
+    "tiny-1024x1024": dict(n=N_TINY, wdtype="f16", wblock=256, shard=1, qwz_out="f16", gblock=128, fanins=[2],
+                           gout="f32"),
+    "gpt-1.3b-layer": dict(n=N_13B, wdtype="bf16", wblock=256, shard=8, qwz_out="bf16", gblock=128, fanins=[8],
+                           gout="f32"),
+    "gpt-20b-layer": dict(n=N_20B, wdtype="bf16", wblock=256, shard=8, qwz_out="bf16", gblock=128, fanins=[8],
+                          gout="f32"),
+    "gpt-20b-3level": dict(n=N_20B, wdtype=None, wblock=None, shard=None, qwz_out=None, gblock=128,
+                           fanins=[2, 4, 48], gout="f32"),
+    "outlier-edge-123456789": dict(n=N_EDGE, wdtype="f32", wblock=256, shard=1, qwz_out="bf16", gblock=64, fanins=[],
+                                   gout="bf16"),
 }

@@ -12,7 +12,7 @@ inputs (the oracle is fast enough to compute whole tensors).
   4  GPT-20B layer, three levels P = 2, 4, 48, final dequant to fp32
   5  123,456,789-element fp32 stress tensor (Student-t nu=3 x0.02, 0.1% x100
      outliers, zero groups), INT8 B=256 and INT4 B=64, dequant to bf16
-  all-shares mode of the reduce level (m = n): P = 2 at config 1's size,
+  all-shares mode of the reduce level (m = n): P = 2 at the tiny workload's size,
      P = 8 over the whole GPT-20B layer
 """
 import numpy as np
@@ -26,6 +26,9 @@ from tests.gpu_util import assert_bits_equal, from_dev, poisoned, to_dev
 
 pytestmark = pytest.mark.gpu
 
+# seed namespace of each workload (the first element of its generator keys) -> its name
+NAMES = {1: "tiny-1024x1024", 2: "gpt-1.3b-layer", 3: "gpt-20b-layer", 4: "gpt-20b-3level", 5: "outlier-edge"}
+
 TORCH_DT = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
 
@@ -37,7 +40,7 @@ def _nsc(n, b):
     return (n + b - 1) // b
 
 
-def _qwz_case(cfg, x, dtype, block, shard, out):
+def _qwz_case(wid, x, dtype, block, shard, out):
     """Quantise the shard (written into its slot of the gathered buffer) and
     dequantise the whole gathered layer, as the bench step does."""
     n = x.size
@@ -50,24 +53,24 @@ def _qwz_case(cfg, x, dtype, block, shard, out):
     y = zq.qwz_dequantize(codes, scales, block, out_dtype=TORCH_DT[out])
     torch.cuda.synchronize()
     oc, os_ = oracle.qwz_quantize(x, block, dtype)
-    assert_bits_equal(from_dev(codes), oc, f"cfg{cfg} qwz codes", block)
-    assert_bits_equal(from_dev(scales), os_, f"cfg{cfg} qwz scales")
+    assert_bits_equal(from_dev(codes), oc, f"{NAMES[wid]} qwz codes", block)
+    assert_bits_equal(from_dev(scales), os_, f"{NAMES[wid]} qwz scales")
     sc, ss = oracle.qwz_quantize(x[:s], block, dtype)
-    assert_bits_equal(from_dev(codes[:s]), sc, f"cfg{cfg} qwz shard codes", block)
-    assert_bits_equal(from_dev(scales[:_nsc(s, block)]), ss, f"cfg{cfg} qwz shard scales")
+    assert_bits_equal(from_dev(codes[:s]), sc, f"{NAMES[wid]} qwz shard codes", block)
+    assert_bits_equal(from_dev(scales[:_nsc(s, block)]), ss, f"{NAMES[wid]} qwz shard scales")
     del codes, scales, xd
-    assert_bits_equal(from_dev(y), oracle.qwz_dequantize(oc, os_, block, out), f"cfg{cfg} qwz dequant -> {out}")
+    assert_bits_equal(from_dev(y), oracle.qwz_dequantize(oc, os_, block, out), f"{NAMES[wid]} qwz dequant -> {out}")
 
 
-def _qgz_chain_case(cfg, n, fanins, block, out, rank=0):
+def _qgz_chain_case(wid, n, fanins, block, out, rank=0):
     """Own gradient quantised on the GPU; each level's receive buffer holds
     chunk `rank` of the previous level's output plus seeded peer chunks."""
-    own = wl.normal_f32(n, 1e-3, key=[cfg, wl.ROLE_OWN_GRAD, 0, 0])
+    own = wl.normal_f32(n, 1e-3, key=[wid, wl.ROLE_OWN_GRAD, 0, 0])
     gp, gs = zq.qgz_quantize(to_dev(own), block)
     op_, os_ = oracle.qgz_quantize(own, block)
     torch.cuda.synchronize()
-    assert_bits_equal(from_dev(gp), op_, f"cfg{cfg} qgz packed", block // 2)
-    assert_bits_equal(from_dev(gs), os_, f"cfg{cfg} qgz scales")
+    assert_bits_equal(from_dev(gp), op_, f"{NAMES[wid]} qgz packed", block // 2)
+    assert_bits_equal(from_dev(gs), os_, f"{NAMES[wid]} qgz scales")
     del own
     cur_gp, cur_gs, cur_op, cur_os, cur_m = gp, gs, op_, os_, n
     for k, P in enumerate(fanins):
@@ -83,81 +86,81 @@ def _qgz_chain_case(cfg, n, fanins, block, out, rank=0):
                 opin[p * mb:(p + 1) * mb] = cur_op[rank * mb:(rank + 1) * mb]
                 osin[p * ms:(p + 1) * ms] = cur_os[rank * ms:(rank + 1) * ms]
             else:
-                xs = wl.normal_f32(m, 1e-3, key=[cfg, wl.ROLE_PEER_GRAD, k, p])
+                xs = wl.normal_f32(m, 1e-3, key=[wid, wl.ROLE_PEER_GRAD, k, p])
                 zq.qgz_quantize(to_dev(xs), block, packed=pin[p * mb:(p + 1) * mb], scales=sin[p * ms:(p + 1) * ms])
                 a, b = oracle.qgz_quantize(xs, block)
                 opin[p * mb:(p + 1) * mb], osin[p * ms:(p + 1) * ms] = a, b
         rp, rs = zq.qgz_reduce_level(pin, sin, P, m, block)
         orp, ors = oracle.qgz_reduce_level(opin, osin, P, m, block)
         torch.cuda.synchronize()
-        assert_bits_equal(from_dev(rp), orp, f"cfg{cfg} level {k} (P={P}) packed", block // 2)
-        assert_bits_equal(from_dev(rs), ors, f"cfg{cfg} level {k} (P={P}) scales")
+        assert_bits_equal(from_dev(rp), orp, f"{NAMES[wid]} level {k} (P={P}) packed", block // 2)
+        assert_bits_equal(from_dev(rs), ors, f"{NAMES[wid]} level {k} (P={P}) scales")
         del pin, sin, opin, osin
         cur_gp, cur_gs, cur_op, cur_os, cur_m = rp, rs, orp, ors, m
     y = zq.qgz_dequantize(cur_gp, cur_gs, cur_m, block, out_dtype=TORCH_DT[out])
     torch.cuda.synchronize()
-    assert_bits_equal(from_dev(y), oracle.qgz_dequantize(cur_op, cur_os, cur_m, block, out), f"cfg{cfg} final dequant")
+    assert_bits_equal(from_dev(y), oracle.qgz_dequantize(cur_op, cur_os, cur_m, block, out), f"{NAMES[wid]} final dequant")
 
 
-def test_config1_tiny():
-    c = wl.CONFIGS[1]
-    w = wl.weights(c["n"], "f16", key=[1, wl.ROLE_WEIGHT, 0, 0])
+def test_tiny_1024x1024():
+    n = wl.WORKLOADS["tiny-1024x1024"]["n"]
+    w = wl.weights(n, "f16", key=[1, wl.ROLE_WEIGHT, 0, 0])
     _qwz_case(1, w, "f16", 256, 1, "f16")
-    _qgz_chain_case(1, c["n"], [2], 128, "f32")
+    _qgz_chain_case(1, n, [2], 128, "f32")
 
 
-def test_config2_gpt13b_layer():
-    c = wl.CONFIGS[2]
-    w = wl.weights(c["n"], "bf16", key=[2, wl.ROLE_WEIGHT, 0, 0])
+def test_gpt13b_layer():
+    n = wl.WORKLOADS["gpt-1.3b-layer"]["n"]
+    w = wl.weights(n, "bf16", key=[2, wl.ROLE_WEIGHT, 0, 0])
     _qwz_case(2, w, "bf16", 256, 8, "bf16")
     del w
-    _qgz_chain_case(2, c["n"], [8], 128, "f32")
+    _qgz_chain_case(2, n, [8], 128, "f32")
 
 
-def test_config3_gpt20b_layer_weights():
+def test_gpt20b_layer_weights():
     w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
     _qwz_case(3, w, "bf16", 256, 8, "bf16")
 
 
-def test_config3_sec_degree_2():
+def test_gpt20b_sec_degree_2():
     """The paper's degree-2 weight partition (primary over a GCD pair, Sec-Degree=2
     secondary): a 1/2 shard quantised into its slot, the 2-shard gather dequantised."""
     w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
     _qwz_case(3, w, "bf16", 256, 2, "bf16")
 
 
-def test_config3_gpt20b_layer_gradients():
+def test_gpt20b_layer_gradients():
     _qgz_chain_case(3, wl.N_20B, [8], 128, "f32")
 
 
-def test_config4_gpt20b_three_levels():
+def test_gpt20b_three_levels():
     _qgz_chain_case(4, wl.N_20B, [2, 4, 48], 128, "f32")
 
 
-def _all_shares_case(cfg, P, m, block):
+def _all_shares_case(wid, P, m, block):
     """All-shares mode of a reduce level: P slices of the whole tensor (m = n),
     random INT4 codes (all 16 nibble values) and scales in the range an
     N(0, 1e-3) gradient gives."""
-    pin = wl.random_bytes(P * _nb4(m), key=[cfg, wl.ROLE_MISC, 9, 0])
-    sin = wl.uniform_f32(P * _nsc(m, block), *wl.ALL_SHARES_SCALES, key=[cfg, wl.ROLE_MISC, 9, 1])
+    pin = wl.random_bytes(P * _nb4(m), key=[wid, wl.ROLE_MISC, 9, 0])
+    sin = wl.uniform_f32(P * _nsc(m, block), *wl.ALL_SHARES_SCALES, key=[wid, wl.ROLE_MISC, 9, 1])
     rp, rs = zq.qgz_reduce_level(torch.from_numpy(pin).cuda(), torch.from_numpy(sin).cuda(), P, m, block)
     torch.cuda.synchronize()
     orp, ors = oracle.qgz_reduce_level(pin, sin, P, m, block)
-    assert_bits_equal(from_dev(rp), orp, f"cfg{cfg} all-shares P={P} packed", block // 2)
-    assert_bits_equal(from_dev(rs), ors, f"cfg{cfg} all-shares P={P} scales")
+    assert_bits_equal(from_dev(rp), orp, f"{NAMES[wid]} all-shares P={P} packed", block // 2)
+    assert_bits_equal(from_dev(rs), ors, f"{NAMES[wid]} all-shares P={P} scales")
 
 
-def test_config1_all_shares():
+def test_tiny_all_shares():
     _all_shares_case(1, 2, wl.N_TINY, 128)
 
 
-def test_config3_all_shares_p8():
+def test_gpt20b_all_shares_p8():
     """P = 8 slices of the whole GPT-20B layer (2.17 GB moved)."""
     _all_shares_case(3, 8, wl.N_20B, 128)
 
 
 @pytest.mark.parametrize("variant", ["int8-b256", "int4-b64"])
-def test_config5_outliers(variant):
+def test_outlier_edge_123456789(variant):
     x = wl.outlier_tensor(wl.N_EDGE, key=[5, wl.ROLE_WEIGHT, 0, 0])
     n = x.size
     if variant == "int8-b256":
@@ -165,15 +168,15 @@ def test_config5_outliers(variant):
         y = zq.qwz_dequantize(codes, scales, 256, out_dtype=torch.bfloat16)
         torch.cuda.synchronize()
         oc, os_ = oracle.qwz_quantize(x, 256)
-        assert_bits_equal(from_dev(codes), oc, "cfg5 int8 codes", 256)
-        assert_bits_equal(from_dev(scales), os_, "cfg5 int8 scales")
+        assert_bits_equal(from_dev(codes), oc, "outlier-edge int8 codes", 256)
+        assert_bits_equal(from_dev(scales), os_, "outlier-edge int8 scales")
         assert int((os_ == 0).sum()) >= n // 256 // 100, "zero groups must give zero scales"
-        assert_bits_equal(from_dev(y), oracle.qwz_dequantize(oc, os_, 256, "bf16"), "cfg5 int8 dequant bf16")
+        assert_bits_equal(from_dev(y), oracle.qwz_dequantize(oc, os_, 256, "bf16"), "outlier-edge int8 dequant bf16")
     else:
         packed, scales = zq.qgz_quantize(to_dev(x), 64)
         y = zq.qgz_dequantize(packed, scales, n, 64, out_dtype=torch.bfloat16)
         torch.cuda.synchronize()
         op_, os_ = oracle.qgz_quantize(x, 64)
-        assert_bits_equal(from_dev(packed), op_, "cfg5 int4 packed", 32)
-        assert_bits_equal(from_dev(scales), os_, "cfg5 int4 scales")
-        assert_bits_equal(from_dev(y), oracle.qgz_dequantize(op_, os_, n, 64, "bf16"), "cfg5 int4 dequant bf16")
+        assert_bits_equal(from_dev(packed), op_, "outlier-edge int4 packed", 32)
+        assert_bits_equal(from_dev(scales), os_, "outlier-edge int4 scales")
+        assert_bits_equal(from_dev(y), oracle.qgz_dequantize(op_, os_, n, 64, "bf16"), "outlier-edge int4 dequant bf16")
