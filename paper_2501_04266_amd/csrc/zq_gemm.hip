@@ -21,7 +21,8 @@
 //                ping-pong schedule, waves w and w + 4 of a SIMD half a K-step
 //                apart (one stores the next tile and reads its fragments
 //                while the other runs its MFMAs, with its loads and
-//                dequantisation in between); buffer loads, none predicated.
+//                dequantisation in between); buffer loads, none predicated;
+//                K split across workgroups when the tiles are few and K long.
 //   k_dqgemm     few rows: 64 x 64 tiles over 4 waves with RS register sets
 //                of loads in flight and K split across workgroups when the
 //                tiles alone are too few; also the many-row fallback for
@@ -66,6 +67,18 @@ constexpr int kDqGemmTileN = ZQ_GEMM_BN;  // columns of y per workgroup
 constexpr int kDqGemmK = 64;              // K must be a multiple of this
 constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
 constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 21;  // 32-bit buffer offsets in the ping-pong kernel
+// K splits of the ping-pong kernel when its tiles leave CUs idle
+#ifndef ZQ_GEMM_PP_MAX_SPLITS
+#define ZQ_GEMM_PP_MAX_SPLITS 8
+#endif
+#ifndef ZQ_GEMM_PP_MIN_SPLIT_STEPS
+#define ZQ_GEMM_PP_MIN_SPLIT_STEPS 96
+#endif
+#ifndef ZQ_GEMM_PP_SPLIT_GAIN
+#define ZQ_GEMM_PP_SPLIT_GAIN 10
+#endif
+constexpr int64_t kDqGemmMaxSplits = ZQ_GEMM_PP_MAX_SPLITS;
+constexpr int64_t kDqGemmMinSplitSteps = ZQ_GEMM_PP_MIN_SPLIT_STEPS;
 // few rows (M <= this): 64 x 64 tiles over 4 waves, K split across
 // workgroups when the tiles alone cannot fill the GPU
 #ifndef ZQ_GEMM_SMALL_M
@@ -355,11 +368,15 @@ __device__ __forceinline__ void phase_end() {
   __builtin_amdgcn_sched_barrier(0);
 }
 
-template <int XT>
+// SPLIT: workgroup w takes K-steps [s KT / splits, (s + 1) KT / splits) of
+// tile w mod T (s = w / T) and adds its partial tile into y, which the host
+// has zeroed; used when the tiles alone would leave much of the GPU idle in
+// the last round.
+template <int XT, bool SPLIT>
 __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                   const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
                                                   int lgB, float* __restrict__ y, int64_t mtiles, int64_t ntiles,
-                                                  int /*splits*/) {
+                                                  int splits) {
   constexpr int BM = 256, BN = 256, WN = 4, NT = 512;
   constexpr int TI = 4, TJ = 2;                  // 32 x 32 MFMA tiles per wave (128 x 64)
   constexpr int XC = BM * kBK / 8 / NT;          // 4 x chunks per thread and K-step
@@ -369,7 +386,7 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
   __shared__ u32x4 Bs[2][BN * kLDK / 8];
 
   const int64_t T = mtiles * ntiles;
-  const int64_t wg = blockIdx.x;
+  const int64_t wg = SPLIT ? blockIdx.x % T : blockIdx.x;
   const int64_t q = T / kXcds, r = T % kXcds, xcd = wg % kXcds, idx = wg / kXcds;
   const int64_t t = !ZQ_GEMM_XCD_MAP ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
   const int64_t per_group = (int64_t)kGroupM * ntiles;
@@ -380,7 +397,10 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
   const int64_t m0 = mt * BM, n0 = nt * BN;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
-  const int KT = (int)(K / kBK);
+  const int KTall = (int)(K / kBK);
+  const int split = SPLIT ? (int)(blockIdx.x / T) : 0;
+  const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
+  const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
 
   // tile kt + 1 is held in registers from its loads (phases of K-step kt - 1)
   // to its LDS store (phases of K-step kt): part P of a tile is x chunks 2P,
@@ -418,7 +438,7 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
       __builtin_amdgcn_make_buffer_rsrc((void*)(scales + s0), (short)0, (int)((s1 - s0) * 4), kBufferFlags);
   auto gload = [&](int kt, auto part_c) {
     constexpr int R = 0, P = decltype(part_c)::value;
-    const int k0 = kt * kBK;
+    const int k0 = (kt0 + kt) * kBK;
 #pragma unroll
     for (int i = 2 * P; i < 2 * P + 2; ++i)
       xrs[R][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xres, (int)xoff[i], 2 * k0, 0));
@@ -566,7 +586,10 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t m = m0 + wm * TI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (m < M && n < N) y[m * N + n] = acc[i][j][e];
+        if (m < M && n < N) {
+          if constexpr (SPLIT) atomicAdd(y + m * N + n, acc[i][j][e]);
+          else y[m * N + n] = acc[i][j][e];
+        }
       }
     }
 }
@@ -581,7 +604,10 @@ static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads && 64 * 2 * 2 == kD
 
 // pp: the large tile's ping-pong kernel, for K <= kDqGemmPpMaxK
 DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
-  if (!small && ZQ_GEMM_PINGPONG && pp) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16> : &k_dqgemm_pp<ZQ_F16>;
+  if (!small && ZQ_GEMM_PINGPONG && pp) {
+    if (split) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, true> : &k_dqgemm_pp<ZQ_F16, true>;
+    return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, false> : &k_dqgemm_pp<ZQ_F16, false>;
+  }
   if (!small)
     return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
                          : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
@@ -590,6 +616,33 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
                          : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>;
   return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>
                        : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>;
+}
+
+// K splits for the 256 x 256 tiles.  A tile's workgroup fills a CU (its LDS
+// buffers alone take 147 KB), so the tiles run in rounds of one workgroup per
+// CU, and a last round that is mostly empty idles much of the GPU (96 tiles
+// on 256 CUs run at 37% use).  Splitting K s ways makes s times as many
+// workgroups of 1/s the work; the count taken minimises the rounds' cost
+// ceil(tiles s / CUs) / s, with each split at least kDqGemmMinSplitSteps
+// K-steps and a split required to win by ZQ_GEMM_PP_SPLIT_GAIN percent (it
+// adds a zero fill of y and atomic additions).
+int64_t large_splits(int64_t tiles, int64_t ksteps) {
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+    cus = 256;
+  int64_t most = ksteps / kDqGemmMinSplitSteps;
+  if (most > kDqGemmMaxSplits) most = kDqGemmMaxSplits;
+  int64_t best = 1;
+  double best_cost = (double)((tiles + cus - 1) / cus);
+  for (int64_t s = 2; s <= most; ++s) {
+    const double cost = (double)((tiles * s + cus - 1) / cus) / (double)s * (1.0 + ZQ_GEMM_PP_SPLIT_GAIN / 100.0);
+    if (cost < best_cost) {
+      best = s;
+      best_cost = cost;
+    }
+  }
+  return best;
 }
 
 }  // namespace
@@ -615,9 +668,17 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
   const uint16_t* xh = static_cast<const uint16_t*>(x);
   if (M > ZQ_GEMM_SMALL_M) {
     const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
-    if (mtiles * ntiles > kMaxGrid) return ZQ_E_SIZE;
-    return launch(dqgemm_kernel(xt, false, false, K <= kDqGemmPpMaxK), (unsigned)(mtiles * ntiles), kDqGemmThreads,
-                  st, xh, codes, scales, M, N, K, lgB, y, mtiles, ntiles, 1);
+    const int64_t tiles = mtiles * ntiles;
+    const bool pp = K <= kDqGemmPpMaxK;
+    const int64_t splits = pp ? large_splits(tiles, K / kDqGemmK) : 1;
+    if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
+    if (splits > 1) {
+      const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
+      int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
+      if (rc != ZQ_OK) return rc;
+    }
+    return launch(dqgemm_kernel(xt, false, splits > 1, pp), (unsigned)(tiles * splits), kDqGemmThreads, st, xh,
+                  codes, scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
   }
   // few rows: small tiles, and K split across workgroups (partial tiles added
   // into a zeroed y) when the tiles alone cannot fill the GPU

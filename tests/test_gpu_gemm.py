@@ -129,6 +129,25 @@ def test_gpt20b_layer_gemms_sampled_rows():
         off += N * K
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K,B", [(600, 300, 12288, 256), (700, 300, 24576, 128)])
+def test_dequant_gemm_large_tiles_split_k(M, N, K, B, dtype):
+    """Few 256 x 256 tiles with a long K: the host splits K across workgroups
+    (2 and 4 ways here) that add their partial tiles into a zeroed y.  x = a/4
+    with |a| <= 4 keeps every partial sum a multiple of 2^-9 below 2^15, so
+    the result is exact in any order of the additions."""
+    rng = np.random.default_rng(M + K)
+    x = wl.to_storage((rng.integers(-4, 5, M * K) / 4.0).astype(np.float32), dtype).reshape(M, K)
+    codes = rng.integers(-127, 128, N * K).astype(np.int8)
+    scales = np.full(-(-(N * K) // B), 2.0 ** -7, np.float32)
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, dtype)
+    y = zq.qwz_dequant_gemm(_x_dev(x, dtype), to_dev(codes), to_dev(scales), N, B)
+    torch.cuda.synchronize()
+    got = from_dev(y).astype(np.float64)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
+
+
 @pytest.mark.parametrize("K", [1 << 21, (1 << 21) + 256])
 def test_dequant_gemm_long_k(K):
     """Reductions as long as 2^21 take the ping-pong schedule (32-bit lane
