@@ -93,7 +93,24 @@ constexpr int kDqGemmSmallTile = 64;
 #endif
 constexpr int kDqGemmSmallRsets = ZQ_GEMM_SMALL_RSETS;  // register sets (K-steps of loads ahead) of the small tiles
 constexpr int kDqGemmSmallThreads = 256;
-constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // workgroups a split launch aims for
+constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // waves / 4 a split launch aims for
+// K groups per few-row workgroup (KG of k_dqgemm), taken where K is a
+// multiple of 64 * KG and a split launch would make at least
+// ZQ_GEMM_SMALL_KG_ATOMICS / 1000 atomic additions into y per weight byte
+// and row tile (M * splits / (K * mtiles); each weight byte is dequantised and
+// multiplied once per row tile).  The additions, about one L2 operation each
+// (~330 G/s measured), then take a good part of the call, and halving them
+// outweighs the larger workgroup's cost: measured +7-30% at ratios of 0.08 and
+// above, 2-9% slower at 0.04 and below
+#ifndef ZQ_GEMM_SMALL_KG
+#define ZQ_GEMM_SMALL_KG 2
+#endif
+#ifndef ZQ_GEMM_SMALL_KG_ATOMICS
+#define ZQ_GEMM_SMALL_KG_ATOMICS 75
+#endif
+constexpr int kDqGemmSmallKG = ZQ_GEMM_SMALL_KG;
+constexpr int64_t kDqGemmSmallKGAtomics = ZQ_GEMM_SMALL_KG_ATOMICS;
+static_assert(kDqGemmSmallKG == 1 || kDqGemmSmallKG == 2, "few-row K groups");
 using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
                               int64_t, int64_t, int);
 
@@ -145,22 +162,29 @@ __device__ __forceinline__ uint32_t narrow2(float a, float b) {
 
 // BM x BN tile of y per workgroup, WM x WN waves, each wave a (BM/WM) x (BN/WN)
 // block of 32 x 32 MFMA tiles.
+// KG > 1: KG groups of WM x WN waves split each K-step of KG * 64 between them
+// (group h takes its h-th 64-wide part, with LDS buffers of its own) and the
+// groups' partial tiles are summed through LDS at the end, in group order:
+// the split-K of the few-row tiles with KG times fewer splits across
+// workgroups, hence KG times fewer atomic additions into y, at the same
+// number of waves.
 // SPLIT: workgroup w takes K-steps [s KT / splits, (s + 1) KT / splits) of
 // tile w / splits (s = w % splits) and adds its partial tile into y, which the
 // host has zeroed; used when there are too few tiles to fill the GPU.
-template <int XT, int BM, int BN, int WM, int WN, bool SPLIT, int RS = ZQ_GEMM_RSETS>
-__global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+template <int XT, int BM, int BN, int WM, int WN, bool SPLIT, int RS = ZQ_GEMM_RSETS, int KG = 1>
+__global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                          const float* __restrict__ scales, int64_t M, int64_t N,
                                                          int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
                                                          int64_t ntiles, int splits) {
-  constexpr int NT = 64 * WM * WN;                         // threads
+  constexpr int NT = 64 * WM * WN;                         // threads of a K group
   constexpr int TI = BM / WM / 32, TJ = BN / WN / 32;      // MFMA tiles per wave
   constexpr int XC = BM * kBK / 8 / NT;                    // x chunks (8 elements) per thread
   constexpr int WC = BN * kBK / 16 / NT;                   // code chunks (16 codes) per thread
   static_assert(TI >= 1 && TJ >= 1 && XC >= 1 && WC >= 1 && XC * NT * 8 == BM * kBK && WC * NT * 16 == BN * kBK,
                 "tile shape");
-  __shared__ u32x4 As[2][BM * kLDK / 8];
-  __shared__ u32x4 Bs[2][BN * kLDK / 8];
+  static_assert(KG == 1 || KG == 2, "K groups");
+  __shared__ u32x4 As[2][KG][BM * kLDK / 8];
+  __shared__ u32x4 Bs[2][KG][BN * kLDK / 8];
 
   // workgroup -> tile: XCD-contiguous ranges (workgroups are dealt to the
   // XCDs round robin), then column-major groups of kGroupM tile rows
@@ -175,8 +199,9 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
   const int64_t nt = (t % per_group) / gsize;
   const int64_t m0 = mt * BM, n0 = nt * BN;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
-  const int KTall = (int)(K / kBK);
+  const int tid = threadIdx.x % NT, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
+  const int kh = KG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);  // K group
+  const int KTall = (int)(K / (kBK * KG));
   const int split = SPLIT ? (int)(blockIdx.x % splits) : 0;
   const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
   const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
@@ -193,7 +218,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
     u32x4(&xr)[XC] = xrs[R];
     u32x4(&wr)[WC] = wrs[R];
     float(&sr)[WC] = srs[R];
-    const int64_t k0 = (int64_t)(kt0 + kt) * kBK;
+    const int64_t k0 = (int64_t)(kt0 + kt) * kBK * KG + kh * kBK;
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
@@ -223,7 +248,7 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      As[buf][(row * kLDK + col) / 8] = xr[i];
+      As[buf][kh][(row * kLDK + col) / 8] = xr[i];
     }
 #pragma unroll
     for (int i = 0; i < WC; ++i) {
@@ -237,8 +262,8 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
         const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * sr[i];
         o[j] = narrow2<XT>(v0, v1);
       }
-      Bs[buf][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
-      Bs[buf][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
+      Bs[buf][kh][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
+      Bs[buf][kh][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
     }
   };
 
@@ -258,9 +283,9 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
     for (int kk = 0; kk < kBK / 16; ++kk) {
       u32x4 a[TI], b[TJ];
 #pragma unroll
-      for (int i = 0; i < TI; ++i) a[i] = As[buf][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int i = 0; i < TI; ++i) a[i] = As[buf][kh][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) b[j] = Bs[buf][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int j = 0; j < TJ; ++j) b[j] = Bs[buf][kh][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -331,6 +356,31 @@ __global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restr
       }
       __syncthreads();
     });
+  }
+
+  if constexpr (KG == 2) {
+    // group 1's partial tile goes through LDS (the operand buffers, whose last
+    // reads completed before the loop's final barrier) and group 0 adds it
+    // to its own, element by element in the same lane and register
+    static_assert(TI * TJ * 16 * NT * 4 <= (int)sizeof(As), "reduction buffer");
+    float* red = reinterpret_cast<float*>(&As[0][0][0]);
+    __syncthreads();
+    if (kh == 1) {
+#pragma unroll
+      for (int i = 0; i < TI; ++i)
+#pragma unroll
+        for (int j = 0; j < TJ; ++j)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) red[((i * TJ + j) * 16 + e) * NT + tid] = acc[i][j][e];
+    }
+    __syncthreads();
+    if (kh == 1) return;
+#pragma unroll
+    for (int i = 0; i < TI; ++i)
+#pragma unroll
+      for (int j = 0; j < TJ; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + red[((i * TJ + j) * 16 + e) * NT + tid];
   }
 
   // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32
@@ -602,8 +652,9 @@ __global__ void __launch_bounds__(256) k_fill_zero(float* __restrict__ y, int64_
 static_assert(!ZQ_GEMM_PINGPONG || (kDqGemmTileM == 256 && kDqGemmTileN == 256 && kDqGemmThreads == 512), "ping-pong tile");
 static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads && 64 * 2 * 2 == kDqGemmSmallThreads, "launch shape");
 
-// pp: the large tile's ping-pong kernel, for K <= kDqGemmPpMaxK
-DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
+// pp: the large tile's ping-pong kernel, for K <= kDqGemmPpMaxK; kg: the
+// few-row kernel with kDqGemmSmallKG K groups
+DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp, bool kg = false) {
   if (!small && ZQ_GEMM_PINGPONG && pp) {
     if (split) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, true> : &k_dqgemm_pp<ZQ_F16, true>;
     return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, false> : &k_dqgemm_pp<ZQ_F16, false>;
@@ -611,6 +662,12 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp) {
   if (!small)
     return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
                          : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
+  constexpr int S = kDqGemmSmallTile, R = kDqGemmSmallRsets, G = kDqGemmSmallKG;
+  if (kg) {
+    if (split)
+      return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, S, S, 2, 2, true, R, G> : &k_dqgemm<ZQ_F16, S, S, 2, 2, true, R, G>;
+    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, S, S, 2, 2, false, R, G> : &k_dqgemm<ZQ_F16, S, S, 2, 2, false, R, G>;
+  }
   if (split)
     return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>
                          : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>;
@@ -681,20 +738,31 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
                   codes, scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
   }
   // few rows: small tiles, and K split across workgroups (partial tiles added
-  // into a zeroed y) when the tiles alone cannot fill the GPU
+  // into a zeroed y) when the tiles alone cannot fill the GPU; with K groups
+  // a workgroup has kDqGemmSmallKG times the waves and takes K-steps of
+  // kDqGemmSmallKG * 64
   const int64_t mtiles = (M + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
   const int64_t ntiles = (N + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
-  const int64_t tiles = mtiles * ntiles, ksteps = K / kDqGemmK;
-  int64_t splits = (kDqGemmSplitTarget + tiles - 1) / tiles;
-  if (splits > ksteps) splits = ksteps;
-  if (splits < 1) splits = 1;
+  const int64_t tiles = mtiles * ntiles;
+  auto plan = [&](int g) {
+    const int64_t ksteps = K / (g * kDqGemmK);
+    int64_t s = (kDqGemmSplitTarget / g + tiles - 1) / tiles;
+    if (s > ksteps) s = ksteps;
+    return s < 1 ? (int64_t)1 : s;
+  };
+  int64_t splits = plan(1);
+  const bool kg = kDqGemmSmallKG > 1 && K % (kDqGemmSmallKG * kDqGemmK) == 0 && splits > 1 &&
+                  1000 * M * splits >= kDqGemmSmallKGAtomics * K * mtiles;
+  const int G = kg ? kDqGemmSmallKG : 1;
+  if (kg) splits = plan(G);
   if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
+  const unsigned threads = (unsigned)(G * kDqGemmSmallThreads);
   if (splits == 1)
-    return launch(dqgemm_kernel(xt, true, false, false), (unsigned)tiles, kDqGemmSmallThreads, st, xh, codes, scales,
-                  M, N, K, lgB, y, mtiles, ntiles, 1);
+    return launch(dqgemm_kernel(xt, true, false, false, kg), (unsigned)tiles, threads, st, xh, codes, scales, M, N, K,
+                  lgB, y, mtiles, ntiles, 1);
   const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
   int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
   if (rc != ZQ_OK) return rc;
-  return launch(dqgemm_kernel(xt, true, true, false), (unsigned)(tiles * splits), kDqGemmSmallThreads, st, xh, codes,
-                scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
+  return launch(dqgemm_kernel(xt, true, true, false, kg), (unsigned)(tiles * splits), threads, st, xh, codes, scales,
+                M, N, K, lgB, y, mtiles, ntiles, (int)splits);
 }
