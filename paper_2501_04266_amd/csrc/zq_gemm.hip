@@ -25,7 +25,9 @@
 //                K split across workgroups when the tiles are few and K long.
 //   k_dqgemm     few rows: 64 x 64 tiles over 4 waves with RS register sets
 //                of loads in flight and K split across workgroups when the
-//                tiles alone are too few; also the many-row fallback for
+//                tiles alone are too few (two groups of 4 waves on alternate
+//                halves of a 128-wide K-step where the splits' atomic
+//                additions would dominate); also the many-row fallback for
 //                K > kDqGemmPpMaxK (256 x 256, two sets).
 // Many-row workgroups are numbered so that each XCD receives a contiguous
 // range of tiles, and within it groups of 4 tile rows share their weight
