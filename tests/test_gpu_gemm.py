@@ -86,6 +86,30 @@ def test_dequant_gemm_realistic(M, N, K, B, dtype):
     _check_bound(from_dev(y), x, codes, scales, N, B, dtype, f"M={M} N={N} K={K} B={B} {dtype}")
 
 
+@pytest.mark.parametrize("shift", [1, 2, 3])
+@pytest.mark.parametrize("M,N,K", [(5, 70, 320), (40, 100, 1024), (600, 300, 12288)])
+def test_dequant_gemm_split_y_not_16_byte_aligned(M, N, K, shift):
+    """Split launches first zero y, then add partial tiles into it; y placed
+    4, 8 or 12 bytes past a 16-byte boundary (the C ABI asks only 4-byte
+    alignment of y), inside a poisoned buffer: the result is exact and no
+    float outside y changes.
+    (5, 70, 320) and (40, 100, 1024) split K on the few-row path, the second
+    with two K groups; (600, 300, 12288) on the 256 x 256 path."""
+    x, codes, scales = _exact_inputs(M, N, K, 256, "bf16", 4 * M + shift)
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, 256, "bf16")
+    buf = poisoned(M * N + 8, torch.float32)
+    guard = buf.clone()
+    y = buf[shift:shift + M * N].view(M, N)
+    assert y.data_ptr() % 16 == 4 * shift
+    zq.qwz_dequant_gemm(_x_dev(x, "bf16"), to_dev(codes), to_dev(scales), N, 256, y=y)
+    torch.cuda.synchronize()
+    got = from_dev(y).astype(np.float64)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
+    outside = torch.cat([buf[:shift], buf[shift + M * N:]]).view(torch.int32)
+    assert torch.equal(outside, torch.cat([guard[:shift], guard[shift + M * N:]]).view(torch.int32))
+
+
 def test_dequant_gemm_k_zero_and_empty():
     x = torch.zeros((5, 0), dtype=torch.bfloat16, device="cuda")
     codes = torch.zeros(16, dtype=torch.int8, device="cuda")
