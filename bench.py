@@ -337,6 +337,7 @@ def load_valu(call):
 
 GEMM_TOKENS = 8192
 SMALL_TOKENS = 64
+DECODE_TOKENS = 16
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 
 
@@ -382,26 +383,31 @@ def gemm_figures(L, reps, log):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / reps
 
-    # the same GEMMs over few rows (SMALL_TOKENS), where the weight stream
-    # dominates: fused vs separate
-    xs_small = {K: xs[K][:SMALL_TOKENS] for K in (h, 4 * h)}
-    ys_small = {name: torch.empty((SMALL_TOKENS, N), device="cuda", dtype=torch.float32) for name, N, _ in shapes}
-
-    def fused_small():
-        for name, N, K, c, sc in slices:
-            zq.qwz_dequant_gemm(xs_small[K], c, sc, N, B, y=ys_small[name])
-
-    def separate_small():
-        zq.qwz_dequantize(L.codes, L.wscales, B, y=L.y)
-        o = 0
-        for name, N, K, _, _ in slices:
-            F.linear(xs_small[K], L.y[o:o + N * K].view(N, K))
-            o += N * K
-
-    small = {"tokens": SMALL_TOKENS, "fused_ms": round(timed(fused_small), 4),
-             "separate_ms": round(timed(separate_small), 4)}
+    # the same GEMMs over few rows, where the weight stream dominates: fused
+    # vs separate, at SMALL_TOKENS (the tiled few-row kernel) and DECODE_TOKENS
+    # (the weight-streaming kernel)
     wbytes = L.codes.numel() + 4 * L.wscales.numel()
-    small["fused_weight_GBps"] = round(wbytes / (small["fused_ms"] * 1e-3) / 1e9, 1)
+
+    def few_rows(T):
+        xs_small = {K: xs[K][:T] for K in (h, 4 * h)}
+        ys_small = {name: torch.empty((T, N), device="cuda", dtype=torch.float32) for name, N, _ in shapes}
+
+        def fused_small():
+            for name, N, K, c, sc in slices:
+                zq.qwz_dequant_gemm(xs_small[K], c, sc, N, B, y=ys_small[name])
+
+        def separate_small():
+            zq.qwz_dequantize(L.codes, L.wscales, B, y=L.y)
+            o = 0
+            for name, N, K, _, _ in slices:
+                F.linear(xs_small[K], L.y[o:o + N * K].view(N, K))
+                o += N * K
+
+        r = {"tokens": T, "fused_ms": round(timed(fused_small), 4), "separate_ms": round(timed(separate_small), 4)}
+        r["fused_weight_GBps"] = round(wbytes / (r["fused_ms"] * 1e-3) / 1e9, 1)
+        return r
+
+    small, decode = few_rows(SMALL_TOKENS), few_rows(DECODE_TOKENS)
 
     flops = sum(2 * M * N * K for _, N, K in shapes)
     f_ms, s_ms = timed(fused), timed(separate)
@@ -417,7 +423,7 @@ def gemm_figures(L, reps, log):
             "per_gemm_TFLOPs": per,
             "separate_dequant_plus_torch_gemm_ms": round(s_ms, 3),
             "separate_TFLOPs": round(flops / (s_ms * 1e-3) / 1e12, 1),
-            "few_tokens": small}
+            "few_tokens": small, "decode_tokens": decode}
 
 
 def cpu_model():

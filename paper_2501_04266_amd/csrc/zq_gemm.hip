@@ -29,6 +29,9 @@
 //                halves of a 128-wide K-step where the splits' atomic
 //                additions would dominate); also the many-row fallback for
 //                K > kDqGemmPpMaxK (256 x 256, two sets).
+//   k_dqgemv     M <= 16: weight streaming on 16 x 16 x 32 MFMAs, codes loaded
+//                straight into the operand registers, x staged in LDS once
+//                per K range (see the kernel).
 // Many-row workgroups are numbered so that each XCD receives a contiguous
 // range of tiles, and within it groups of 4 tile rows share their weight
 // tiles through that XCD's L2.
@@ -112,6 +115,14 @@ constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // waves / 4 a split l
 #endif
 constexpr int kDqGemmSmallKG = ZQ_GEMM_SMALL_KG;
 constexpr int64_t kDqGemmSmallKGAtomics = ZQ_GEMM_SMALL_KG_ATOMICS;
+// M <= 16: the weight-streaming kernel k_dqgemv, aiming at this many workgroups
+#ifndef ZQ_GEMM_GEMV
+#define ZQ_GEMM_GEMV 1
+#endif
+#ifndef ZQ_GEMM_GEMV_TARGET
+#define ZQ_GEMM_GEMV_TARGET 1024
+#endif
+constexpr int64_t kGemvTargetWgs = ZQ_GEMM_GEMV_TARGET;
 static_assert(kDqGemmSmallKG == 1 || kDqGemmSmallKG == 2, "few-row K groups");
 using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
                               int64_t, int64_t, int);
@@ -121,6 +132,7 @@ namespace {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 constexpr int kBK = 64;
 // buffer resource word 3 for raw (untyped) buffer loads on gfx9-family targets
@@ -646,6 +658,111 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
     }
 }
 
+// Few tokens (M <= kGemvRows): a weight-streaming kernel on
+// v_mfma_f32_16x16x32.  Workgroup (g, s) takes weight rows [64 g, 64 g + 64),
+// 16 per wave, and the K range [s kc, min(K, (s + 1) kc)), kc <= kGemvKc.
+// Within each 256-wide chunk of that range, lane l (row l % 16 of its wave's
+// 16, lane group h = l / 16) loads the 64 codes k = 64 h .. 64 h + 63 of its
+// row straight from memory, and its 8 operand codes of MFMA t are
+// k = 64 h + 8 t .. 64 h + 8 t + 7; x's fragments are read from LDS with the
+// same mapping, so each MFMA sums the same products as the plain order would,
+// grouped differently.  All chunks of a wave's range are loaded before any is
+// used (16 KB per wave), x's rows over the range are staged into LDS once,
+// and the loop has no barrier.  Rows M .. 15 of the x slab, and its columns
+// past the range, are zero.
+constexpr int kGemvRows = 16;   // x rows (M <= kGemvRows)
+constexpr int kGemvKc = 1024;   // longest K range of a workgroup
+
+template <int XT>
+__device__ __forceinline__ f32x4_t mfma16(u32x4 a, u32x4 b, f32x4_t c) {
+  if constexpr (XT == ZQ_BF16)
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a), __builtin_bit_cast(bf16x8_t, b),
+                                                   c, 0, 0, 0);
+  else
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c,
+                                                  0, 0, 0);
+}
+
+template <int XT, bool SPLIT>
+__global__ void __launch_bounds__(256) k_dqgemv(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+                                                const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
+                                                int lgB, float* __restrict__ y, int64_t ngroups, int kc) {
+  constexpr int NC = kGemvKc / 256, G16 = kGemvKc / 8;  // chunks per wave at most; 16-byte granules per slab row
+  // x slab: row m, granule q (elements 8 q .. 8 q + 7 of the range) at
+  // m * G16 + (q ^ m): the 16 rows' granules of one fragment read then fall
+  // in 16 distinct 16-byte bank groups
+  __shared__ u32x4 xs[kGemvRows * G16];
+  const int64_t grp = blockIdx.x % ngroups, split = blockIdx.x / ngroups;
+  const int64_t kb = split * kc, ke = K - kb < kc ? K : kb + kc;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r = lane & 15, h = lane >> 4;
+  const int64_t n = grp * 64 + wave * 16 + r;
+
+  // codes and scales of every chunk (a 64-code segment is 64-aligned in the
+  // flat index, so it spans at most two blocks of B >= 32: codes 0-31 and
+  // 32-63 take scales 0 and 1)
+  u32x4 cw[NC][4];
+  float sc[NC][2];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    const int64_t k = kb + 256 * c + 64 * h;
+    if (n < N && k < ke) {
+      const int64_t f = n * K + k;
+      const u32x4* p = reinterpret_cast<const u32x4*>(codes + f);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cw[c][j] = p[j];
+      sc[c][0] = scales[f >> lgB];
+      sc[c][1] = scales[(f + 32) >> lgB];
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) cw[c][j] = u32x4{0u, 0u, 0u, 0u};
+      sc[c][0] = sc[c][1] = 0.0f;
+    }
+  }
+  // every granule of the slab is written (zero past the range), so the
+  // fragments of a partly covered chunk read zeros, never stale LDS
+  for (int i = tid; i < kGemvRows * G16; i += 256) {
+    const int m = i / G16, q = i % G16;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (m < M && kb + 8 * q < ke) v = *reinterpret_cast<const u32x4*>(x + m * K + kb + 8 * q);
+    xs[m * G16 + (q ^ m)] = v;
+  }
+  __syncthreads();
+
+  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if (kb + 256 * c >= ke) break;  // workgroup-uniform
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      const u32x4 wv = cw[c][t >> 1];
+      const uint32_t w0 = (t & 1) ? wv.z : wv.x, w1 = (t & 1) ? wv.w : wv.y;
+      const float s = sc[c][t >> 2];
+      uint32_t b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t w = u < 2 ? w0 : w1;
+        const int sh = (u & 1) * 16;
+        const float v0 = (float)(int32_t)(int8_t)(w >> sh) * s;
+        const float v1 = (float)(int32_t)(int8_t)(w >> (sh + 8)) * s;
+        b[u] = narrow2<XT>(v0, v1);
+      }
+      const int q = 32 * c + 8 * h + t;
+      acc = mfma16<XT>(xs[r * G16 + (q ^ r)], u32x4{b[0], b[1], b[2], b[3]}, acc);
+    }
+  }
+  // D register e of lane l: row 4 (l / 16) + e, column l % 16
+  if (n < N) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int64_t m = 4 * h + e;
+      if (m < M) {
+        if constexpr (SPLIT) atomicAdd(y + m * N + n, acc[e]);
+        else y[m * N + n] = acc[e];
+      }
+    }
+  }
+}
+
 // y[0, count) = 0 (for the split kernel, which adds into y)
 __global__ void __launch_bounds__(256) k_fill_zero(float* __restrict__ y, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < count; i += (int64_t)gridDim.x * 256) y[i] = 0.0f;
@@ -738,6 +855,23 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
     }
     return launch(dqgemm_kernel(xt, false, splits > 1, pp), (unsigned)(tiles * splits), kDqGemmThreads, st, xh,
                   codes, scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
+  }
+  if (ZQ_GEMM_GEMV && M <= kGemvRows) {
+    // few tokens: the weight-streaming kernel; the K range per workgroup
+    // halves (down to 256) until about kGemvTargetWgs workgroups run
+    const int64_t ngroups = (N + 63) / 64;
+    int64_t kc = kGemvKc;
+    while (kc > 256 && ngroups * ((K + kc - 1) / kc) < kGemvTargetWgs) kc /= 2;
+    const int64_t splits = K > kc ? (K + kc - 1) / kc : 1;
+    if (ngroups * splits > kMaxGrid) return ZQ_E_SIZE;
+    if (splits == 1)
+      return launch(xt == ZQ_BF16 ? &k_dqgemv<ZQ_BF16, false> : &k_dqgemv<ZQ_F16, false>, (unsigned)ngroups, 256u, st,
+                    xh, codes, scales, M, N, K, lgB, y, ngroups, (int)kc);
+    const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
+    int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
+    if (rc != ZQ_OK) return rc;
+    return launch(xt == ZQ_BF16 ? &k_dqgemv<ZQ_BF16, true> : &k_dqgemv<ZQ_F16, true>, (unsigned)(ngroups * splits),
+                  256u, st, xh, codes, scales, M, N, K, lgB, y, ngroups, (int)kc);
   }
   // few rows: small tiles, and K split across workgroups (partial tiles added
   // into a zeroed y) when the tiles alone cannot fill the GPU; with K groups

@@ -56,6 +56,29 @@ def test_dequant_gemm_exact(M, N, K, B, dtype):
     assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
 
 
+# M <= 16: the weight-streaming kernel (codes straight into the 16 x 16 x 32
+# MFMA operands, x staged in LDS over K ranges of up to 1024): ragged N, K
+# that ends inside a 256-wide chunk (64, 192, 320, 1088) or inside a
+# workgroup's range (4160), one and several ranges per row group, ranges of
+# 256, 512 (N = 32768) and 1024 (N = 65600), every block size (B = 32: two
+# blocks per 64-code segment)
+DECODE = [(1, 1, 64, 32), (2, 70, 192, 64), (7, 129, 320, 128), (15, 1000, 1088, 256), (16, 64, 4160, 1024),
+          (16, 4100, 2048, 32), (3, 32768, 960, 512), (16, 65600, 1088, 64)]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("M,N,K,B", DECODE)
+def test_dequant_gemm_decode_exact(M, N, K, B, dtype):
+    x, codes, scales = _exact_inputs(M, N, K, B, dtype, 31 * M + N + K)
+    want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, dtype)
+    y = poisoned(M * N, torch.float32).reshape(M, N)
+    zq.qwz_dequant_gemm(_x_dev(x, dtype), to_dev(codes), to_dev(scales), N, B, y=y)
+    torch.cuda.synchronize()
+    got = from_dev(y).astype(np.float64)
+    bad = np.flatnonzero(got != want)
+    assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
+
+
 def _check_bound(got, x, codes, scales, N, B, dtype, what):
     want = oracle.qwz_dequant_gemm(x, codes, scales, N, B, dtype)
     K = x.shape[1]
