@@ -222,11 +222,12 @@ def test_dequant_gemm_long_k(K):
     assert bad.size == 0, f"{bad.size} of {got.size} differ; first at {np.unravel_index(bad[0], got.shape)}"
 
 
-@pytest.mark.parametrize("M", [64, 640])
+@pytest.mark.parametrize("M", [8, 64, 640])
 def test_dequant_gemm_graph_capture(M):
-    """The GEMM (both the few-row split path, which also launches its own
-    zero fill, and the large-tile path) only enqueues kernels, so it replays
-    from a HIP graph; exact inputs make every replay bit-identical."""
+    """The GEMM only enqueues kernels, so it replays from a HIP graph: the
+    weight-streaming path (M = 8) and the few-row tiles with two K groups
+    (M = 64), both split (each also launches its own zero fill), and the
+    large-tile path (M = 640); exact inputs make every replay bit-identical."""
     N, K, B = 384, 2048, 256
     x, codes, scales = _exact_inputs(M, N, K, B, "bf16", 31 + M)
     xd, cd, sd = _x_dev(x, "bf16"), to_dev(codes), to_dev(scales)
