@@ -154,10 +154,11 @@ int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* co
  * i.e. w is exactly what qwz_dequantize(codes, scales, N*K, block, ., xt)
  * writes, and the sum is taken in binary32 by the matrix cores in an order of
  * their own, always within 2*K*2^-24 * sum_k |x[m][k] w[n][k]| of the exact
- * value.  For M <= 512, and for larger M when the output tiles are few and K
- * is long (at least 12288), the K range may be split across workgroups whose
- * partial sums are added into y atomically (after the library zeroes y), so
- * such results can differ between runs in their last bits.
+ * value.  When the output tiles alone would leave much of the GPU idle (few
+ * rows, or a few hundred rows with few tiles), the K range may be split across
+ * workgroups whose partial sums are added into y atomically (after the
+ * library zeroes y), so such results can differ between runs in their last
+ * bits.
  *   x       [M][K] row-major, xt = ZQ_BF16 or ZQ_F16 (read)
  *   codes   [N][K] int8 row-major (a PyTorch Linear weight, flattened), scales
  *           [ceil(N*K/block)] floats (read)

@@ -74,20 +74,26 @@ constexpr int kDqGemmThreads = 64 * ZQ_GEMM_WM * ZQ_GEMM_WN;
 constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 21;  // 32-bit buffer offsets in the ping-pong kernel
 // K splits of the ping-pong kernel when its tiles leave CUs idle
 #ifndef ZQ_GEMM_PP_MAX_SPLITS
-#define ZQ_GEMM_PP_MAX_SPLITS 8
+#define ZQ_GEMM_PP_MAX_SPLITS 16
 #endif
-#ifndef ZQ_GEMM_PP_MIN_SPLIT_STEPS
-#define ZQ_GEMM_PP_MIN_SPLIT_STEPS 96
+// the split model's two costs: one 64-wide K-step of a 256 x 256 tile on one
+// CU, and one atomic addition into y with the GPU's others (measured: a K-step
+// 1.3-1.7 us, atomic additions about 330 G/s)
+#ifndef ZQ_GEMM_PP_STEP_NS
+#define ZQ_GEMM_PP_STEP_NS 1500
 #endif
-#ifndef ZQ_GEMM_PP_SPLIT_GAIN
-#define ZQ_GEMM_PP_SPLIT_GAIN 10
+#ifndef ZQ_GEMM_ATOMIC_PS
+#define ZQ_GEMM_ATOMIC_PS 3
 #endif
 constexpr int64_t kDqGemmMaxSplits = ZQ_GEMM_PP_MAX_SPLITS;
-constexpr int64_t kDqGemmMinSplitSteps = ZQ_GEMM_PP_MIN_SPLIT_STEPS;
-// few rows (M <= this): 64 x 64 tiles over 4 waves, K split across
-// workgroups when the tiles alone cannot fill the GPU
+// few rows (M <= this; M <= 16 takes the weight-streaming kernel): 64 x 64
+// tiles over 4 waves, K split across workgroups when the tiles alone cannot
+// fill the GPU.  Above it the 256 x 256 tiles with the split model of
+// large_splits were faster: over the layer's four GEMMs 0.25 against 0.31 ms
+// at 80 tokens, 0.55 against 1.00 at 512, while the small tiles won at 48-64
+// (0.21 against 0.23)
 #ifndef ZQ_GEMM_SMALL_M
-#define ZQ_GEMM_SMALL_M 512
+#define ZQ_GEMM_SMALL_M 64
 #endif
 #ifndef ZQ_GEMM_SPLIT_TARGET
 #define ZQ_GEMM_SPLIT_TARGET 2048
@@ -796,26 +802,31 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp, bool kg = fa
 
 // K splits for the 256 x 256 tiles.  A tile's workgroup fills a CU (its LDS
 // buffers alone take 147 KB), so the tiles run in rounds of one workgroup per
-// CU, and a last round that is mostly empty idles much of the GPU (96 tiles
-// on 256 CUs run at 37% use).  Splitting K s ways makes s times as many
-// workgroups of 1/s the work; the count taken minimises the rounds' cost
-// ceil(tiles s / CUs) / s, with each split at least kDqGemmMinSplitSteps
-// K-steps and a split required to win by ZQ_GEMM_PP_SPLIT_GAIN percent (it
-// adds a zero fill of y and atomic additions).
-int64_t large_splits(int64_t tiles, int64_t ksteps) {
+// CU, and a last round that is mostly empty idles much of the GPU (72 tiles
+// on 256 CUs use 28% of it).  Splitting K s ways makes s times as many
+// workgroups of 1/s the K-steps, at the price of a zero fill of y and
+// M N s atomic additions; the count taken minimises the modelled time
+//   ceil(tiles s / CUs) ceil(ksteps / s) step  +  [s > 1] M N s atomic
+// (step, atomic: ZQ_GEMM_PP_STEP_NS, ZQ_GEMM_ATOMIC_PS), which splits the
+// GEMMs of a few hundred rows 2-16 ways and leaves full rounds whole.
+int64_t large_splits(int64_t tiles, int64_t ksteps, int64_t M, int64_t N) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
-  int64_t most = ksteps / kDqGemmMinSplitSteps;
-  if (most > kDqGemmMaxSplits) most = kDqGemmMaxSplits;
+  const int64_t most = ksteps < kDqGemmMaxSplits ? ksteps : kDqGemmMaxSplits;
+  const double step = ZQ_GEMM_PP_STEP_NS * 1e-9, atomic = ZQ_GEMM_ATOMIC_PS * 1e-12;
+  auto cost = [&](int64_t s) {
+    const double rounds = (double)((tiles * s + cus - 1) / cus), steps = (double)((ksteps + s - 1) / s);
+    return rounds * steps * step + (s > 1 ? (double)M * (double)N * (double)s * atomic : 0.0);
+  };
   int64_t best = 1;
-  double best_cost = (double)((tiles + cus - 1) / cus);
+  double best_cost = cost(1);
   for (int64_t s = 2; s <= most; ++s) {
-    const double cost = (double)((tiles * s + cus - 1) / cus) / (double)s * (1.0 + ZQ_GEMM_PP_SPLIT_GAIN / 100.0);
-    if (cost < best_cost) {
+    const double c = cost(s);
+    if (c < best_cost) {
       best = s;
-      best_cost = cost;
+      best_cost = c;
     }
   }
   return best;
@@ -827,7 +838,7 @@ int64_t large_splits(int64_t tiles, int64_t ksteps) {
 using namespace zq;
 
 // qwz_dequant_gemm (include/zq.h): argument checks, then one launch (or a
-// zero fill and a split-K launch for few rows)
+// zero fill and a split-K launch when the tiles are few)
 int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const float* scales, int64_t M, int64_t N,
                      int64_t K, int32_t block, float* y, void* stream) {
   if (M < 0 || N < 0 || K < 0) return ZQ_E_SIZE;
@@ -846,7 +857,7 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
     const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
     const int64_t tiles = mtiles * ntiles;
     const bool pp = K <= kDqGemmPpMaxK;
-    const int64_t splits = pp ? large_splits(tiles, K / kDqGemmK) : 1;
+    const int64_t splits = pp ? large_splits(tiles, K / kDqGemmK, M, N) : 1;
     if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
     if (splits > 1) {
       const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;

@@ -36,11 +36,13 @@ def _exact_inputs(M, N, K, B, dtype, seed):
     return x, codes, scales
 
 
-# M <= 512: the few-row path; M > 512: the 256 x 256 tile path, with ragged
-# edges in M and N and 1, 2, 3 and 10 K-steps of 64
-EXACT = [(1, 1, 64, 256), (37, 100, 192, 32), (128, 128, 64, 256), (300, 257, 1024, 128), (129, 383, 640, 64),
-         (256, 512, 6144, 256), (600, 300, 64, 256), (513, 257, 128, 64), (777, 520, 192, 32),
-         (1024, 512, 640, 128)]
+# M <= 16: the weight-streaming kernel; 17-64: the few-row tiles (K split,
+# with two K groups where K % 128 == 0 and the splits are many); M > 64: the
+# 256 x 256 tiles, K split when they are few (down to one K-step per split);
+# ragged edges in M and N and 1, 2, 3 and 10 K-steps of 64
+EXACT = [(1, 1, 64, 256), (37, 100, 192, 32), (17, 70, 320, 64), (40, 300, 1024, 256), (64, 129, 2048, 128),
+         (128, 128, 64, 256), (300, 257, 1024, 128), (129, 383, 640, 64), (256, 512, 6144, 256),
+         (600, 300, 64, 256), (513, 257, 128, 64), (777, 520, 192, 32), (1024, 512, 640, 128)]
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
@@ -91,8 +93,8 @@ def _check_bound(got, x, codes, scales, N, B, dtype, what):
     return float((err / np.maximum(mag, 1e-300)).max())
 
 
-# M <= 512 takes the small-tile path, with K split across workgroups when the
-# tiles alone are too few (all of these but the last)
+# M <= 16 the weight-streaming kernel, 17-64 the few-row tiles, larger M the
+# 256 x 256 tiles; all but (1, 128, 64, 32) split K across workgroups
 REAL = [(256, 384, 6144, 256), (100, 130, 1024, 64), (64, 256, 24576, 256), (1, 128, 64, 32),
         (16, 24576, 6144, 256), (200, 6144, 24576, 256), (257, 640, 1024, 128), (513, 256, 1024, 256)]
 
@@ -180,7 +182,7 @@ def test_gpt20b_layer_gemms_sampled_rows():
 @pytest.mark.parametrize("M,N,K,B", [(600, 300, 12288, 256), (700, 300, 24576, 128)])
 def test_dequant_gemm_large_tiles_split_k(M, N, K, B, dtype):
     """Few 256 x 256 tiles with a long K: the host splits K across workgroups
-    (2 and 4 ways here) that add their partial tiles into a zeroed y.  x = a/4
+    (16 ways here) that add their partial tiles into a zeroed y.  x = a/4
     with |a| <= 4 keeps every partial sum a multiple of 2^-9 below 2^15, so
     the result is exact in any order of the additions."""
     rng = np.random.default_rng(M + K)
