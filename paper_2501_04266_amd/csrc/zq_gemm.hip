@@ -14,24 +14,22 @@
 // binary32 and summed in binary32 by the MFMA units (v_mfma_f32_32x32x16_bf16
 // / _f16), in an order the hardware fixes.
 //
-// Kernels (all tile y with 32 x 32 MFMA tiles, K advancing 64 at a time,
-// LDS rows padded by 16 bytes so that the 16-byte fragment reads of 16
-// consecutive lanes fall in distinct banks):
-//   k_dqgemm_pp  many rows: 256 x 256 tiles over 8 waves (128 x 64 each) in a
-//                ping-pong schedule, waves w and w + 4 of a SIMD half a K-step
-//                apart (one stores the next tile and reads its fragments
-//                while the other runs its MFMAs, with its loads and
-//                dequantisation in between); buffer loads, none predicated;
-//                K split across workgroups when the tiles are few and K long.
-//   k_dqgemm     few rows: 64 x 64 tiles over 4 waves with RS register sets
-//                of loads in flight and K split across workgroups when the
-//                tiles alone are too few (two groups of 4 waves on alternate
-//                halves of a 128-wide K-step where the splits' atomic
-//                additions would dominate); also the many-row fallback for
-//                K > kDqGemmPpMaxK (256 x 256, two sets).
+// Kernels:
 //   k_dqgemv     M <= 16: weight streaming on 16 x 16 x 32 MFMAs, codes loaded
 //                straight into the operand registers, x staged in LDS once
 //                per K range (see the kernel).
+//   k_dqgemm_pp  M > 16: 256 x 256 tiles (128 x 256 up to 128 rows) over 8
+//                waves in a ping-pong schedule, waves w and w + 4 of a SIMD
+//                half a K-step apart (one stores the next tile and reads its
+//                fragments while the other runs its MFMAs, with its loads
+//                and dequantisation in between); buffer loads, none
+//                predicated; K split across workgroups where the tiles are
+//                too few to fill the GPU.
+//   k_dqgemm     the same 256 x 256 tiles in a plain two-stage schedule with
+//                64-bit addresses, for K > kDqGemmPpMaxK.
+// The tiled kernels use 32 x 32 MFMA tiles, K advancing 64 at a time, LDS
+// rows padded by 16 bytes so that the 16-byte fragment reads of 16
+// consecutive lanes fall in distinct banks.
 // Many-row workgroups are numbered so that each XCD receives a contiguous
 // range of tiles, and within it groups of 4 tile rows share their weight
 // tiles through that XCD's L2.
@@ -61,9 +59,6 @@ namespace zq {
 #ifndef ZQ_GEMM_WN
 #define ZQ_GEMM_WN 4
 #endif
-#ifndef ZQ_GEMM_RSETS
-#define ZQ_GEMM_RSETS 2
-#endif
 #ifndef ZQ_GEMM_PINGPONG
 #define ZQ_GEMM_PINGPONG 1
 #endif
@@ -86,50 +81,21 @@ constexpr int64_t kDqGemmPpMaxK = int64_t(1) << 21;  // 32-bit buffer offsets in
 #define ZQ_GEMM_ATOMIC_PS 3
 #endif
 constexpr int64_t kDqGemmMaxSplits = ZQ_GEMM_PP_MAX_SPLITS;
-// few rows (M <= this; M <= 16 takes the weight-streaming kernel): 64 x 64
-// tiles over 4 waves, K split across workgroups when the tiles alone cannot
-// fill the GPU.  Above it the 256 x 256 tiles with the split model of
-// large_splits were faster: over the layer's four GEMMs 0.25 against 0.31 ms
-// at 80 tokens, 0.55 against 1.00 at 512, while the small tiles won at 48-64
-// (0.21 against 0.23)
-#ifndef ZQ_GEMM_SMALL_M
-#define ZQ_GEMM_SMALL_M 64
+// Row ranges: M <= 16 the weight-streaming kernel k_dqgemv; up to
+// ZQ_GEMM_HALF_M rows the ping-pong kernel's 128 x 256 tiles; beyond, its
+// 256 x 256 tiles.  Measured over the layer's four GEMMs in sequence: the
+// streaming kernel 0.11-0.15 ms at 1-16 tokens against 0.17 for the ping-pong
+// kernel; the 128 x 256 tiles 10-14% faster than the 256 x 256 at 65-128
+// rows and slower at 144-224; and both faster than a 64 x 64 few-row tile
+// kernel (since removed) from 24 rows on.
+#ifndef ZQ_GEMM_HALF_M
+#define ZQ_GEMM_HALF_M 128
 #endif
-#ifndef ZQ_GEMM_SPLIT_TARGET
-#define ZQ_GEMM_SPLIT_TARGET 2048
-#endif
-constexpr int kDqGemmSmallTile = 64;
-#ifndef ZQ_GEMM_SMALL_RSETS
-#define ZQ_GEMM_SMALL_RSETS 3
-#endif
-constexpr int kDqGemmSmallRsets = ZQ_GEMM_SMALL_RSETS;  // register sets (K-steps of loads ahead) of the small tiles
-constexpr int kDqGemmSmallThreads = 256;
-constexpr int kDqGemmSplitTarget = ZQ_GEMM_SPLIT_TARGET;  // waves / 4 a split launch aims for
-// K groups per few-row workgroup (KG of k_dqgemm), taken where K is a
-// multiple of 64 * KG and a split launch would make at least
-// ZQ_GEMM_SMALL_KG_ATOMICS / 1000 atomic additions into y per weight byte
-// and row tile (M * splits / (K * mtiles); each weight byte is dequantised and
-// multiplied once per row tile).  The additions, about one L2 operation each
-// (~330 G/s measured), then take a good part of the call, and halving them
-// outweighs the larger workgroup's cost: measured +7-30% at ratios of 0.08 and
-// above, 2-9% slower at 0.04 and below
-#ifndef ZQ_GEMM_SMALL_KG
-#define ZQ_GEMM_SMALL_KG 2
-#endif
-#ifndef ZQ_GEMM_SMALL_KG_ATOMICS
-#define ZQ_GEMM_SMALL_KG_ATOMICS 75
-#endif
-constexpr int kDqGemmSmallKG = ZQ_GEMM_SMALL_KG;
-constexpr int64_t kDqGemmSmallKGAtomics = ZQ_GEMM_SMALL_KG_ATOMICS;
-// M <= 16: the weight-streaming kernel k_dqgemv, aiming at this many workgroups
-#ifndef ZQ_GEMM_GEMV
-#define ZQ_GEMM_GEMV 1
-#endif
+// the weight-streaming kernel aims at this many workgroups
 #ifndef ZQ_GEMM_GEMV_TARGET
 #define ZQ_GEMM_GEMV_TARGET 1024
 #endif
 constexpr int64_t kGemvTargetWgs = ZQ_GEMM_GEMV_TARGET;
-static_assert(kDqGemmSmallKG == 1 || kDqGemmSmallKG == 2, "few-row K groups");
 using DqGemmKernel = void (*)(const uint16_t*, const int8_t*, const float*, int64_t, int64_t, int64_t, int, float*,
                               int64_t, int64_t, int);
 
@@ -181,37 +147,29 @@ __device__ __forceinline__ uint32_t narrow2(float a, float b) {
 }
 
 // BM x BN tile of y per workgroup, WM x WN waves, each wave a (BM/WM) x (BN/WN)
-// block of 32 x 32 MFMA tiles.
-// KG > 1: KG groups of WM x WN waves split each K-step of KG * 64 between them
-// (group h takes its h-th 64-wide part, with LDS buffers of its own) and the
-// groups' partial tiles are summed through LDS at the end, in group order:
-// the split-K of the few-row tiles with KG times fewer splits across
-// workgroups, hence KG times fewer atomic additions into y, at the same
-// number of waves.
-// SPLIT: workgroup w takes K-steps [s KT / splits, (s + 1) KT / splits) of
-// tile w / splits (s = w % splits) and adds its partial tile into y, which the
-// host has zeroed; used when there are too few tiles to fill the GPU.
-template <int XT, int BM, int BN, int WM, int WN, bool SPLIT, int RS = ZQ_GEMM_RSETS, int KG = 1>
-__global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
+// block of 32 x 32 MFMA tiles, with plain loads and 64-bit addresses (the
+// schedule for K beyond the ping-pong kernel's 32-bit offsets); `splits` is
+// unused (the launch signature is shared with k_dqgemm_pp).
+template <int XT, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(64 * WM * WN) k_dqgemm(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                          const float* __restrict__ scales, int64_t M, int64_t N,
                                                          int64_t K, int lgB, float* __restrict__ y, int64_t mtiles,
                                                          int64_t ntiles, int splits) {
-  constexpr int NT = 64 * WM * WN;                         // threads of a K group
+  constexpr int NT = 64 * WM * WN;                         // threads
   constexpr int TI = BM / WM / 32, TJ = BN / WN / 32;      // MFMA tiles per wave
   constexpr int XC = BM * kBK / 8 / NT;                    // x chunks (8 elements) per thread
   constexpr int WC = BN * kBK / 16 / NT;                   // code chunks (16 codes) per thread
   static_assert(TI >= 1 && TJ >= 1 && XC >= 1 && WC >= 1 && XC * NT * 8 == BM * kBK && WC * NT * 16 == BN * kBK,
                 "tile shape");
-  static_assert(KG == 1 || KG == 2, "K groups");
-  __shared__ u32x4 As[2][KG][BM * kLDK / 8];
-  __shared__ u32x4 Bs[2][KG][BN * kLDK / 8];
+  __shared__ u32x4 As[2][BM * kLDK / 8];
+  __shared__ u32x4 Bs[2][BN * kLDK / 8];
 
   // workgroup -> tile: XCD-contiguous ranges (workgroups are dealt to the
   // XCDs round robin), then column-major groups of kGroupM tile rows
   const int64_t T = mtiles * ntiles;
-  const int64_t wg = SPLIT ? blockIdx.x / splits : blockIdx.x;
+  const int64_t wg = blockIdx.x;
   const int64_t q = T / kXcds, r = T % kXcds, xcd = wg % kXcds, idx = wg / kXcds;
-  const int64_t t = SPLIT || !ZQ_GEMM_XCD_MAP ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
+  const int64_t t = !ZQ_GEMM_XCD_MAP ? wg : xcd < r ? xcd * (q + 1) + idx : r * (q + 1) + (xcd - r) * q + idx;
   const int64_t per_group = (int64_t)kGroupM * ntiles;
   const int64_t first_m = (t / per_group) * kGroupM;
   const int64_t gsize = mtiles - first_m < kGroupM ? mtiles - first_m : kGroupM;
@@ -219,17 +177,14 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
   const int64_t nt = (t % per_group) / gsize;
   const int64_t m0 = mt * BM, n0 = nt * BN;
 
-  const int tid = threadIdx.x % NT, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
-  const int kh = KG == 1 ? 0 : __builtin_amdgcn_readfirstlane((int)threadIdx.x / NT);  // K group
-  const int KTall = (int)(K / (kBK * KG));
-  const int split = SPLIT ? (int)(blockIdx.x % splits) : 0;
-  const int kt0 = SPLIT ? (int)((int64_t)split * KTall / splits) : 0;
-  const int KT = SPLIT ? (int)((int64_t)(split + 1) * KTall / splits) - kt0 : KTall;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, wm = wave / WN, wn = wave % WN;
+  const int KT = (int)(K / kBK);
+  (void)splits;
 
-  // RS register sets: tile t's loads are issued RS K-steps before its LDS
+  // two register sets: tile t's loads are issued two K-steps before its LDS
   // store
-  u32x4 xrs[RS][XC], wrs[RS][WC];
-  float srs[RS][WC];
+  u32x4 xrs[2][XC], wrs[2][WC];
+  float srs[2][WC];
   // global -> registers: x rows m0.., 8 elements per chunk; codes rows n0..,
   // 16 codes per chunk with the scale of their block (a chunk never straddles
   // a block: chunks are 16-aligned in the flat index and B >= 32)
@@ -238,7 +193,7 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
     u32x4(&xr)[XC] = xrs[R];
     u32x4(&wr)[WC] = wrs[R];
     float(&sr)[WC] = srs[R];
-    const int64_t k0 = (int64_t)(kt0 + kt) * kBK * KG + kh * kBK;
+    const int64_t k0 = (int64_t)kt * kBK;
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
@@ -268,7 +223,7 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
 #pragma unroll
     for (int i = 0; i < XC; ++i) {
       const int c = tid + NT * i, row = c >> 3, col = (c & 7) * 8;
-      As[buf][kh][(row * kLDK + col) / 8] = xr[i];
+      As[buf][(row * kLDK + col) / 8] = xr[i];
     }
 #pragma unroll
     for (int i = 0; i < WC; ++i) {
@@ -282,8 +237,8 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
         const float v1 = (float)(int32_t)(int8_t)(word >> (sh + 8)) * sr[i];
         o[j] = narrow2<XT>(v0, v1);
       }
-      Bs[buf][kh][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
-      Bs[buf][kh][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
+      Bs[buf][(row * kLDK + col) / 8] = u32x4{o[0], o[1], o[2], o[3]};
+      Bs[buf][(row * kLDK + col) / 8 + 1] = u32x4{o[4], o[5], o[6], o[7]};
     }
   };
 
@@ -303,9 +258,9 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
     for (int kk = 0; kk < kBK / 16; ++kk) {
       u32x4 a[TI], b[TJ];
 #pragma unroll
-      for (int i = 0; i < TI; ++i) a[i] = As[buf][kh][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int i = 0; i < TI; ++i) a[i] = As[buf][((wm * TI * 32 + i * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
-      for (int j = 0; j < TJ; ++j) b[j] = Bs[buf][kh][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
+      for (int j = 0; j < TJ; ++j) b[j] = Bs[buf][((wn * TJ * 32 + j * 32 + frow) * kLDK + kk * 16 + fk) / 8];
 #pragma unroll
       for (int i = 0; i < TI; ++i)
 #pragma unroll
@@ -315,92 +270,27 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
 
   using R0 = std::integral_constant<int, 0>;
   using R1 = std::integral_constant<int, 1>;
-  if constexpr (RS == 2) {
-    // tile t lives in register set t % 2 from its load (K-step t - 2) to its
-    // store (end of K-step t - 1)
-    if (KT > 0) {
-      gload(0, R0{});
-      sstore(0, R0{});
-    }
-    if (KT > 1) gload(1, R1{});
-    if (KT > 2) gload(2, R0{});
-    __syncthreads();
-#pragma unroll 1
-    for (int kt = 0; kt < KT; kt += 2) {
-      compute(0);                                   // K-step kt (buffer 0)
-      if (kt + 1 < KT) sstore(1, R1{});             // tile kt + 1
-      if (kt + 3 < KT) gload(kt + 3, R1{});
-      __syncthreads();
-      if (kt + 1 < KT) {
-        compute(1);                                 // K-step kt + 1 (buffer 1)
-        if (kt + 2 < KT) sstore(0, R0{});           // tile kt + 2
-        if (kt + 4 < KT) gload(kt + 4, R0{});
-        __syncthreads();
-      }
-    }
-  } else {
-    // tile t lives in register set t % RS from its loads (K-step t - RS) to
-    // its store (end of K-step t - 1).  Buffer parity and set index repeat
-    // every 2 RS K-steps; the steady-state block has no branches, so each
-    // wait covers exactly the loads it needs.
-    constexpr int U = 2 * RS;
-    if (KT > 0) {
-      gload(0, R0{});
-      sstore(0, R0{});
-    }
-    static_for<1, RS + 1>([&](auto rc) {
-      constexpr int r = decltype(rc)::value;
-      if (r < KT) gload(r, std::integral_constant<int, r % RS>{});
-    });
-    __syncthreads();
-    int kt = 0;
-#pragma unroll 1
-    for (; kt + U + RS + 1 <= KT; kt += U) {
-      static_for<0, U>([&](auto jc) {
-        constexpr int j = decltype(jc)::value;
-        using S = std::integral_constant<int, (j + 1) % RS>;
-        compute(j & 1);
-        sstore((j + 1) & 1, S{});
-        gload(kt + j + 1 + RS, S{});
-        __syncthreads();
-      });
-    }
-    static_for<0, U + RS + 1>([&](auto jc) {
-      constexpr int j = decltype(jc)::value;
-      using S = std::integral_constant<int, (j + 1) % RS>;
-      const int t = kt + j;
-      if (t < KT) {
-        compute(j & 1);
-        if (t + 1 < KT) sstore((j + 1) & 1, S{});
-        if (t + 1 + RS < KT) gload(t + 1 + RS, S{});
-      }
-      __syncthreads();
-    });
+  // tile t lives in register set t % 2 from its load (K-step t - 2) to its
+  // store (end of K-step t - 1)
+  if (KT > 0) {
+    gload(0, R0{});
+    sstore(0, R0{});
   }
-
-  if constexpr (KG == 2) {
-    // group 1's partial tile goes through LDS (the operand buffers, whose last
-    // reads completed before the loop's final barrier) and group 0 adds it
-    // to its own, element by element in the same lane and register
-    static_assert(TI * TJ * 16 * NT * 4 <= (int)sizeof(As), "reduction buffer");
-    float* red = reinterpret_cast<float*>(&As[0][0][0]);
+  if (KT > 1) gload(1, R1{});
+  if (KT > 2) gload(2, R0{});
+  __syncthreads();
+#pragma unroll 1
+  for (int kt = 0; kt < KT; kt += 2) {
+    compute(0);                                   // K-step kt (buffer 0)
+    if (kt + 1 < KT) sstore(1, R1{});             // tile kt + 1
+    if (kt + 3 < KT) gload(kt + 3, R1{});
     __syncthreads();
-    if (kh == 1) {
-#pragma unroll
-      for (int i = 0; i < TI; ++i)
-#pragma unroll
-        for (int j = 0; j < TJ; ++j)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) red[((i * TJ + j) * 16 + e) * NT + tid] = acc[i][j][e];
+    if (kt + 1 < KT) {
+      compute(1);                                 // K-step kt + 1 (buffer 1)
+      if (kt + 2 < KT) sstore(0, R0{});           // tile kt + 2
+      if (kt + 4 < KT) gload(kt + 4, R0{});
+      __syncthreads();
     }
-    __syncthreads();
-    if (kh == 1) return;
-#pragma unroll
-    for (int i = 0; i < TI; ++i)
-#pragma unroll
-      for (int j = 0; j < TJ; ++j)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) acc[i][j][e] = acc[i][j][e] + red[((i * TJ + j) * 16 + e) * NT + tid];
   }
 
   // D register e of lane l: row 8 (e / 4) + 4 (l / 32) + e % 4, column l % 32
@@ -412,10 +302,7 @@ __global__ void __launch_bounds__(64 * WM * WN * KG) k_dqgemm(const uint16_t* __
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t m = m0 + wm * TI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (m < M && n < N) {
-          if constexpr (SPLIT) atomicAdd(y + m * N + n, acc[i][j][e]);
-          else y[m * N + n] = acc[i][j][e];
-        }
+        if (m < M && n < N) y[m * N + n] = acc[i][j][e];
       }
     }
 }
@@ -442,16 +329,19 @@ __device__ __forceinline__ void phase_end() {
 // tile w mod T (s = w / T) and adds its partial tile into y, which the host
 // has zeroed; used when the tiles alone would leave much of the GPU idle in
 // the last round.
-template <int XT, bool SPLIT>
+// TI = 2: 128 x 256 tiles (each wave 64 x 64) for 65-128 rows, where a
+// 256-row tile would multiply zero rows half the time.
+template <int XT, bool SPLIT, int TI = 4>
 __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ x, const int8_t* __restrict__ codes,
                                                   const float* __restrict__ scales, int64_t M, int64_t N, int64_t K,
                                                   int lgB, float* __restrict__ y, int64_t mtiles, int64_t ntiles,
                                                   int splits) {
-  constexpr int BM = 256, BN = 256, WN = 4, NT = 512;
-  constexpr int TI = 4, TJ = 2;                  // 32 x 32 MFMA tiles per wave (128 x 64)
-  constexpr int XC = BM * kBK / 8 / NT;          // 4 x chunks per thread and K-step
+  constexpr int BM = 64 * TI, BN = 256, WN = 4, NT = 512;
+  constexpr int TJ = 2;                          // 32 x 32 MFMA tiles per wave: TI x 2 (128 or 64 x 64)
+  constexpr int XC = BM * kBK / 8 / NT;          // x chunks per thread and K-step (TI)
   constexpr int WC = BN * kBK / 16 / NT;         // 2 code chunks per thread and K-step
-  static_assert(XC == 4 && WC == 2, "tile shape");
+  constexpr int XH = XC / 2;                     // x chunks per part
+  static_assert((TI == 4 || TI == 2) && XC == TI && WC == 2, "tile shape");
   __shared__ u32x4 As[2][BM * kLDK / 8];
   __shared__ u32x4 Bs[2][BN * kLDK / 8];
 
@@ -510,7 +400,7 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
     constexpr int R = 0, P = decltype(part_c)::value;
     const int k0 = (kt0 + kt) * kBK;
 #pragma unroll
-    for (int i = 2 * P; i < 2 * P + 2; ++i)
+    for (int i = XH * P; i < XH * P + XH; ++i)
       xrs[R][i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xres, (int)xoff[i], 2 * k0, 0));
     wrs[R][P] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(wres, (int)woff[P], k0, 0));
     const uint32_t si = (woff[P] + (uint32_t)k0) >> lgB;
@@ -533,7 +423,7 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
   auto store = [&](int buf, auto part_c) {
     constexpr int P = decltype(part_c)::value;
 #pragma unroll
-    for (int i = 2 * P; i < 2 * P + 2; ++i) {
+    for (int i = XH * P; i < XH * P + XH; ++i) {
       const int c = tid + NT * i;
       As[buf][(c >> 3) * kRow16 + (c & 7)] = xrs[0][i];
     }
@@ -580,7 +470,7 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
       for (int i = 0; i < TI; ++i)
 #pragma unroll
         for (int j = 0; j < TJ; ++j) acc[i][j] = mfma32<XT>(fa[i][s], fb[j][s], acc[i][j]);
-    if constexpr (DQ) {
+    if constexpr (DQ && TI == 4) {
       deq(part_c);
       __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // 4 MFMAs first: the codes may still be arriving
 #pragma unroll
@@ -589,6 +479,15 @@ __global__ void __launch_bounds__(512) k_dqgemm_pp(const uint16_t* __restrict__ 
         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // 4 VALU
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    } else if constexpr (DQ) {
+      deq(part_c);  // 8 MFMAs: the same 40 VALU instructions, 8 after each of 5
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+#pragma unroll
+      for (int q = 0; q < 5; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 8, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     }
     (void)P;
   };
@@ -775,29 +674,21 @@ __global__ void __launch_bounds__(256) k_fill_zero(float* __restrict__ y, int64_
 }
 
 static_assert(!ZQ_GEMM_PINGPONG || (kDqGemmTileM == 256 && kDqGemmTileN == 256 && kDqGemmThreads == 512), "ping-pong tile");
-static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads && 64 * 2 * 2 == kDqGemmSmallThreads, "launch shape");
+static_assert(64 * ZQ_GEMM_WM * ZQ_GEMM_WN == kDqGemmThreads, "launch shape");
 
-// pp: the large tile's ping-pong kernel, for K <= kDqGemmPpMaxK; kg: the
-// few-row kernel with kDqGemmSmallKG K groups
-DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp, bool kg = false) {
-  if (!small && ZQ_GEMM_PINGPONG && pp) {
+// pp: the ping-pong kernel (K <= kDqGemmPpMaxK), with 128-row tiles if half;
+// otherwise the plain 256 x 256 kernel, which never splits K
+DqGemmKernel dqgemm_kernel(int xt, bool split, bool pp, bool half) {
+  if (pp && half) {
+    if (split) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, true, 2> : &k_dqgemm_pp<ZQ_F16, true, 2>;
+    return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, false, 2> : &k_dqgemm_pp<ZQ_F16, false, 2>;
+  }
+  if (pp) {
     if (split) return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, true> : &k_dqgemm_pp<ZQ_F16, true>;
     return xt == ZQ_BF16 ? &k_dqgemm_pp<ZQ_BF16, false> : &k_dqgemm_pp<ZQ_F16, false>;
   }
-  if (!small)
-    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>
-                         : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN, false>;
-  constexpr int S = kDqGemmSmallTile, R = kDqGemmSmallRsets, G = kDqGemmSmallKG;
-  if (kg) {
-    if (split)
-      return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, S, S, 2, 2, true, R, G> : &k_dqgemm<ZQ_F16, S, S, 2, 2, true, R, G>;
-    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, S, S, 2, 2, false, R, G> : &k_dqgemm<ZQ_F16, S, S, 2, 2, false, R, G>;
-  }
-  if (split)
-    return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>
-                         : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, true, kDqGemmSmallRsets>;
-  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>
-                       : &k_dqgemm<ZQ_F16, kDqGemmSmallTile, kDqGemmSmallTile, 2, 2, false, kDqGemmSmallRsets>;
+  return xt == ZQ_BF16 ? &k_dqgemm<ZQ_BF16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>
+                       : &k_dqgemm<ZQ_F16, kDqGemmTileM, kDqGemmTileN, ZQ_GEMM_WM, ZQ_GEMM_WN>;
 }
 
 // K splits for the 256 x 256 tiles.  A tile's workgroup fills a CU (its LDS
@@ -809,13 +700,13 @@ DqGemmKernel dqgemm_kernel(int xt, bool small, bool split, bool pp, bool kg = fa
 //   ceil(tiles s / CUs) ceil(ksteps / s) step  +  [s > 1] M N s atomic
 // (step, atomic: ZQ_GEMM_PP_STEP_NS, ZQ_GEMM_ATOMIC_PS), which splits the
 // GEMMs of a few hundred rows 2-16 ways and leaves full rounds whole.
-int64_t large_splits(int64_t tiles, int64_t ksteps, int64_t M, int64_t N) {
+int64_t large_splits(int64_t tiles, int64_t ksteps, int64_t M, int64_t N, double step_scale) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
     cus = 256;
   const int64_t most = ksteps < kDqGemmMaxSplits ? ksteps : kDqGemmMaxSplits;
-  const double step = ZQ_GEMM_PP_STEP_NS * 1e-9, atomic = ZQ_GEMM_ATOMIC_PS * 1e-12;
+  const double step = ZQ_GEMM_PP_STEP_NS * 1e-9 * step_scale, atomic = ZQ_GEMM_ATOMIC_PS * 1e-12;
   auto cost = [&](int64_t s) {
     const double rounds = (double)((tiles * s + cus - 1) / cus), steps = (double)((ksteps + s - 1) / s);
     return rounds * steps * step + (s > 1 ? (double)M * (double)N * (double)s * atomic : 0.0);
@@ -853,21 +744,7 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
     return ZQ_E_ALIAS;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const uint16_t* xh = static_cast<const uint16_t*>(x);
-  if (M > ZQ_GEMM_SMALL_M) {
-    const int64_t mtiles = (M + kDqGemmTileM - 1) / kDqGemmTileM, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
-    const int64_t tiles = mtiles * ntiles;
-    const bool pp = K <= kDqGemmPpMaxK;
-    const int64_t splits = pp ? large_splits(tiles, K / kDqGemmK, M, N) : 1;
-    if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
-    if (splits > 1) {
-      const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
-      int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
-      if (rc != ZQ_OK) return rc;
-    }
-    return launch(dqgemm_kernel(xt, false, splits > 1, pp), (unsigned)(tiles * splits), kDqGemmThreads, st, xh,
-                  codes, scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
-  }
-  if (ZQ_GEMM_GEMV && M <= kGemvRows) {
+  if (M <= kGemvRows) {
     // few tokens: the weight-streaming kernel; the K range per workgroup
     // halves (down to 256) until about kGemvTargetWgs workgroups run
     const int64_t ngroups = (N + 63) / 64;
@@ -884,32 +761,20 @@ int qwz_dequant_gemm(const void* x, zq_dtype xt, const int8_t* codes, const floa
     return launch(xt == ZQ_BF16 ? &k_dqgemv<ZQ_BF16, true> : &k_dqgemv<ZQ_F16, true>, (unsigned)(ngroups * splits),
                   256u, st, xh, codes, scales, M, N, K, lgB, y, ngroups, (int)kc);
   }
-  // few rows: small tiles, and K split across workgroups (partial tiles added
-  // into a zeroed y) when the tiles alone cannot fill the GPU; with K groups
-  // a workgroup has kDqGemmSmallKG times the waves and takes K-steps of
-  // kDqGemmSmallKG * 64
-  const int64_t mtiles = (M + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
-  const int64_t ntiles = (N + kDqGemmSmallTile - 1) / kDqGemmSmallTile;
+  // the ping-pong kernel, K split where its tiles are few; up to
+  // ZQ_GEMM_HALF_M rows with 128 x 256 tiles (a K-step of one costs about 0.6
+  // of a 256 x 256 tile's: half the MFMAs, the same dequantisation)
+  const bool pp = ZQ_GEMM_PINGPONG && K <= kDqGemmPpMaxK, half = pp && M <= ZQ_GEMM_HALF_M;
+  const int64_t bm = half ? kDqGemmTileM / 2 : kDqGemmTileM;
+  const int64_t mtiles = (M + bm - 1) / bm, ntiles = (N + kDqGemmTileN - 1) / kDqGemmTileN;
   const int64_t tiles = mtiles * ntiles;
-  auto plan = [&](int g) {
-    const int64_t ksteps = K / (g * kDqGemmK);
-    int64_t s = (kDqGemmSplitTarget / g + tiles - 1) / tiles;
-    if (s > ksteps) s = ksteps;
-    return s < 1 ? (int64_t)1 : s;
-  };
-  int64_t splits = plan(1);
-  const bool kg = kDqGemmSmallKG > 1 && K % (kDqGemmSmallKG * kDqGemmK) == 0 && splits > 1 &&
-                  1000 * M * splits >= kDqGemmSmallKGAtomics * K * mtiles;
-  const int G = kg ? kDqGemmSmallKG : 1;
-  if (kg) splits = plan(G);
+  const int64_t splits = pp ? large_splits(tiles, K / kDqGemmK, M, N, half ? 0.6 : 1.0) : 1;
   if (tiles * splits > kMaxGrid) return ZQ_E_SIZE;
-  const unsigned threads = (unsigned)(G * kDqGemmSmallThreads);
-  if (splits == 1)
-    return launch(dqgemm_kernel(xt, true, false, false, kg), (unsigned)tiles, threads, st, xh, codes, scales, M, N, K,
-                  lgB, y, mtiles, ntiles, 1);
-  const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
-  int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
-  if (rc != ZQ_OK) return rc;
-  return launch(dqgemm_kernel(xt, true, true, false, kg), (unsigned)(tiles * splits), threads, st, xh, codes, scales,
-                M, N, K, lgB, y, mtiles, ntiles, (int)splits);
+  if (splits > 1) {
+    const int64_t count = M * N, fill_grid = count / 256 + 1 < 4096 ? count / 256 + 1 : 4096;
+    int rc = launch(&k_fill_zero, (unsigned)fill_grid, 256u, st, y, count);
+    if (rc != ZQ_OK) return rc;
+  }
+  return launch(dqgemm_kernel(xt, splits > 1, pp, half), (unsigned)(tiles * splits), kDqGemmThreads, st, xh, codes,
+                scales, M, N, K, lgB, y, mtiles, ntiles, (int)splits);
 }

@@ -36,11 +36,12 @@ def _exact_inputs(M, N, K, B, dtype, seed):
     return x, codes, scales
 
 
-# M <= 16: the weight-streaming kernel; 17-64: the few-row tiles (K split,
-# with two K groups where K % 128 == 0 and the splits are many); M > 64: the
-# 256 x 256 tiles, K split when they are few (down to one K-step per split);
-# ragged edges in M and N and 1, 2, 3 and 10 K-steps of 64
+# M <= 16: the weight-streaming kernel; 17-128: the ping-pong kernel's
+# 128 x 256 tiles; M > 128: its 256 x 256 tiles; K split when the tiles are
+# few (down to one K-step per split); ragged edges in M and N and 1, 2, 3
+# and 10 K-steps of 64
 EXACT = [(1, 1, 64, 256), (37, 100, 192, 32), (17, 70, 320, 64), (40, 300, 1024, 256), (64, 129, 2048, 128),
+         (65, 300, 2048, 64), (100, 520, 6144, 256), (127, 257, 192, 32),
          (128, 128, 64, 256), (300, 257, 1024, 128), (129, 383, 640, 64), (256, 512, 6144, 256),
          (600, 300, 64, 256), (513, 257, 128, 64), (777, 520, 192, 32), (1024, 512, 640, 128)]
 
@@ -93,8 +94,8 @@ def _check_bound(got, x, codes, scales, N, B, dtype, what):
     return float((err / np.maximum(mag, 1e-300)).max())
 
 
-# M <= 16 the weight-streaming kernel, 17-64 the few-row tiles, larger M the
-# 256 x 256 tiles; all but (1, 128, 64, 32) split K across workgroups
+# M <= 16 the weight-streaming kernel, 17-128 the 128 x 256 tiles, larger M
+# the 256 x 256 tiles; all but (1, 128, 64, 32) split K across workgroups
 REAL = [(256, 384, 6144, 256), (100, 130, 1024, 64), (64, 256, 24576, 256), (1, 128, 64, 32),
         (16, 24576, 6144, 256), (200, 6144, 24576, 256), (257, 640, 1024, 128), (513, 256, 1024, 256)]
 
@@ -118,8 +119,8 @@ def test_dequant_gemm_split_y_not_16_byte_aligned(M, N, K, shift):
     4, 8 or 12 bytes past a 16-byte boundary (the C ABI asks only 4-byte
     alignment of y), inside a poisoned buffer: the result is exact and no
     float outside y changes.
-    (5, 70, 320) and (40, 100, 1024) split K on the few-row path, the second
-    with two K groups; (600, 300, 12288) on the 256 x 256 path."""
+    (5, 70, 320) splits K on the weight-streaming path, (40, 100, 1024) on
+    the 128 x 256 tiles, (600, 300, 12288) on the 256 x 256 tiles."""
     x, codes, scales = _exact_inputs(M, N, K, 256, "bf16", 4 * M + shift)
     want = oracle.qwz_dequant_gemm(x, codes, scales, N, 256, "bf16")
     buf = poisoned(M * N + 8, torch.float32)
@@ -227,9 +228,9 @@ def test_dequant_gemm_long_k(K):
 @pytest.mark.parametrize("M", [8, 64, 640])
 def test_dequant_gemm_graph_capture(M):
     """The GEMM only enqueues kernels, so it replays from a HIP graph: the
-    weight-streaming path (M = 8) and the few-row tiles with two K groups
-    (M = 64), both split (each also launches its own zero fill), and the
-    large-tile path (M = 640); exact inputs make every replay bit-identical."""
+    weight-streaming path (M = 8) and the 128 x 256 tiles (M = 64), both
+    split (each also launches its own zero fill), and the 256 x 256 tiles
+    (M = 640); exact inputs make every replay bit-identical."""
     N, K, B = 384, 2048, 256
     x, codes, scales = _exact_inputs(M, N, K, B, "bf16", 31 + M)
     xd, cd, sd = _x_dev(x, "bf16"), to_dev(codes), to_dev(scales)

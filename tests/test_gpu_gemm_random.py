@@ -1,7 +1,7 @@
 """Seeded random sweep of the dequantise-on-load GEMM (qwz_dequant_gemm) over
-its paths -- the weight-streaming kernel (M <= 16), the few-row tiles with
-one or two K groups (17-64), the 256 x 256 ping-pong tile with and without
-K split across workgroups -- with ragged M and N, K up to
+its paths -- the weight-streaming kernel (M <= 16), the ping-pong kernel's
+128 x 256 (17-128 rows) and 256 x 256 tiles, with and without K split across
+workgroups -- with ragged M and N, K up to
 3072, every block size and both input types.  Exact inputs (x = a/4 with
 |a| <= 16, scales 2^-7, so every dequantised weight q/128 and every partial
 sum, a multiple of 2^-9 below 2^15, is exact in binary32) make each case
