@@ -384,8 +384,8 @@ def gemm_figures(L, reps, log):
         return e0.elapsed_time(e1) / reps
 
     # the same GEMMs over few rows, where the weight stream dominates: fused
-    # vs separate, at SMALL_TOKENS (the tiled few-row kernel) and DECODE_TOKENS
-    # (the weight-streaming kernel)
+    # vs separate, at SMALL_TOKENS (the ping-pong kernel's 128-row tiles) and
+    # DECODE_TOKENS (the weight-streaming kernel)
     wbytes = L.codes.numel() + 4 * L.wscales.numel()
 
     def few_rows(T):
