@@ -9,7 +9,8 @@ oracle.  Two kinds of cases:
   binary32 sum in the matrix cores' order is held to
   |y - exact| <= 2 K 2^-24 sum_k |x w| (+ 2^-126 for underflow), the bound for
   any order of K - 1 rounded binary32 additions of exact products.
-Plus the layer's four GEMMs (GPT-20B, 8192 tokens) on sampled rows.
+Plus the layer's four GEMMs (GPT-20B) at 8192 tokens on sampled rows and at
+1, 16, 64 and 1024 tokens.
 """
 import numpy as np
 import pytest
@@ -156,17 +157,23 @@ def test_dequant_gemm_rejects_ragged_k():
         zq.qwz_dequant_gemm(x, codes, scales, 4, 256)
 
 
-def test_gpt20b_layer_gemms_sampled_rows():
-    """The four forward GEMMs of the GPT-20B layer (QKV 3h x h, attention out
-    h x h, FC1 4h x h, FC2 h x 4h; h = 6144) over 8192 tokens, weights taken
-    from the gathered INT8 layer at their offsets; 24 sampled rows of each
-    output against the oracle (the launch configuration the bench times)."""
-    h, M, B = 6144, 8192, 256
+@pytest.fixture(scope="module")
+def gpt20b_layer():
+    """The gathered INT8 GPT-20B layer (oracle-quantised once for the module),
+    on the host and on the device."""
     w = wl.weights(wl.N_20B, "bf16", key=[3, wl.ROLE_WEIGHT, 0, 0])
-    codes, scales = oracle.qwz_quantize(w, B, "bf16")
+    codes, scales = oracle.qwz_quantize(w, 256, "bf16")
     del w
-    dcodes, dscales = to_dev(codes), to_dev(scales)
-    rows = np.unique(np.concatenate([[0, M - 1], np.random.default_rng(9).integers(0, M, 22)]))
+    return codes, scales, to_dev(codes), to_dev(scales)
+
+
+def _layer_gemms(layer, M, rows):
+    """The four forward GEMMs of the GPT-20B layer (QKV 3h x h, attention out
+    h x h, FC1 4h x h, FC2 h x 4h; h = 6144) over M tokens, weights taken from
+    the gathered INT8 layer at their offsets; the given rows of each output
+    against the oracle, within the binary32 accumulation bound."""
+    codes, scales, dcodes, dscales = layer
+    h, B = 6144, 256
     off = 0
     for name, N, K in (("qkv", 3 * h, h), ("attn_out", h, h), ("fc1", 4 * h, h), ("fc2", h, 4 * h)):
         xf = wl.normal_f32(M * K, 1.0, key=[8, wl.ROLE_MISC, 1, K])
@@ -175,8 +182,27 @@ def test_gpt20b_layer_gemms_sampled_rows():
                                 N, B)
         torch.cuda.synchronize()
         got = from_dev(y[torch.from_numpy(rows).cuda()])
-        _check_bound(got, x[rows], codes[off:off + N * K], scales[off // B:(off + N * K) // B], N, B, "bf16", name)
+        _check_bound(got, x[rows], codes[off:off + N * K], scales[off // B:(off + N * K) // B], N, B, "bf16",
+                     f"{name} M={M}")
         off += N * K
+
+
+def test_gpt20b_layer_gemms_sampled_rows(gpt20b_layer):
+    """The layer's four GEMMs over 8192 tokens (the launch configuration the
+    bench times): 24 sampled rows of each output."""
+    M = 8192
+    _layer_gemms(gpt20b_layer, M, np.unique(np.concatenate([[0, M - 1], np.random.default_rng(9).integers(0, M, 22)])))
+
+
+@pytest.mark.parametrize("M", [1, 16, 64, 1024])
+def test_gpt20b_layer_gemms_few_tokens(gpt20b_layer, M):
+    """The same four GEMMs at the token counts of the other kernel paths: the
+    weight-streaming kernel (1, 16), the 128 x 256 tiles with K split (64),
+    the 256 x 256 tiles, split for attention output and FC2 (1024).  Every
+    row up to 32 tokens, else 24 sampled rows."""
+    rows = np.arange(M) if M <= 32 else np.unique(
+        np.concatenate([[0, M - 1], np.random.default_rng(M).integers(0, M, 22)]))
+    _layer_gemms(gpt20b_layer, M, rows)
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
