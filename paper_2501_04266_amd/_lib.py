@@ -234,6 +234,12 @@ def qgz_reduce_level_gather(packed_slices, scale_slices, m, block=128, packed_ou
     for p, (a, b) in enumerate(zip(packed_slices, scale_slices)):
         _need(a, f"packed_slices[{p}]", int4_bytes(m), _U8)
         _need(b, f"scale_slices[{p}]", _nsc(m, block), _F32)
+        # the library reads the slice addresses on the device and cannot check
+        # them itself: the vector path (m % 32 == 0) loads 16 bytes per lane
+        if m % 32 == 0 and _dev(a, f"packed_slices[{p}]") % 16:
+            raise ValueError(f"packed_slices[{p}] must be 16-byte aligned when m % 32 == 0")
+        if _dev(b, f"scale_slices[{p}]") % 4:
+            raise ValueError(f"scale_slices[{p}] must be 4-byte aligned")
     dev = packed_slices[0].device
     if packed_out is None:
         packed_out = torch.empty(int4_bytes(m), dtype=torch.uint8, device=dev)
@@ -243,12 +249,14 @@ def qgz_reduce_level_gather(packed_slices, scale_slices, m, block=128, packed_ou
     _need(scales_out, "scales_out", _nsc(m, block), _F32)
     # the pointer tables live in device memory (the kernel reads them); built
     # here they are allocated on the current stream and, if the call runs on
-    # another, recorded on it so the allocator keeps them until it finishes
+    # another (a torch stream or a raw handle), recorded on it so the
+    # allocator keeps them until the kernel has read them
     if tables is None:
         tab, stab = gather_tables(packed_slices, scale_slices)
-        if stream is not None and hasattr(stream, "cuda_stream"):
-            tab.record_stream(stream)
-            stab.record_stream(stream)
+        if stream is not None:
+            st = stream if hasattr(stream, "cuda_stream") else torch.cuda.ExternalStream(int(stream))
+            tab.record_stream(st)
+            stab.record_stream(st)
     else:
         tab, stab = tables
         _need(tab, "tables[0]", P, (torch.int64,))

@@ -12,6 +12,10 @@
 #include "zq_host.h"
 #include "zq_internal.h"
 
+#ifndef ZQ_FIXED
+#define ZQ_FIXED 1
+#endif
+
 namespace {
 
 using namespace zq;
@@ -123,11 +127,22 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
   const int64_t grid = grid_for(groups, reduce_tiles(shape));
   if (grid == 0 && groups > 0) return ZQ_E_SIZE;
 
+  // P = 2, 4, 8 on large levels: the kernel with the slice count fixed at
+  // compile time (each workgroup takes reduce_fixed_tiles(P) groups)
+  ReduceKernel fixed = (ZQ_FIXED && shape != ReduceShape::kSmall) ? reduce_fixed_kernel(lgB, P, fused ? yt : -1, gather)
+                                                                  : nullptr;
+  // (its groups: the same whole-group range [0, nfull) in its own group size)
+  const int64_t fixed_groups = fixed ? nfull / (kThreads / 64 * (64 / (block / reduce_fixed_elems()))) : 0;
+  const int64_t fixed_grid = fixed ? grid_for(fixed_groups, reduce_fixed_tiles(P)) : 0;
+  if (fixed && fixed_grid == 0 && groups > 0) return ZQ_E_SIZE;
+
   hipStream_t st = static_cast<hipStream_t>(stream);
   if (groups > 0) {
-    int rc = launch(gather ? reduce_gather_kernel(lgB, shape) : reduce_kernel(lgB, shape, fused ? yt : -1),
-                    (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb, nfull, packed_out,
-                    scales_out, y);
+    int rc = fixed ? launch(fixed, (unsigned)fixed_grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb,
+                            nfull, packed_out, scales_out, y)
+                   : launch(gather ? reduce_gather_kernel(lgB, shape) : reduce_kernel(lgB, shape, fused ? yt : -1),
+                            (unsigned)grid, kThreads, st, packed_in, scales_in, (int)P, slice_bytes, nb, nfull,
+                            packed_out, scales_out, y);
     if (rc != ZQ_OK) return rc;
   }
   // remaining blocks (those after the last whole group, including a short

@@ -93,5 +93,12 @@ ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);
 // slices through device tables of P pointers (bytes, scales); INT4 output only
 ReduceKernel reduce_gather_kernel(int lgB, ReduceShape shape);
 ReduceGenericKernel reduce_generic_kernel(bool gather);
+// vector-path kernel with the slice count fixed at compile time, for P = 2, 4
+// or 8 and B = 64, 128 or 256 (ydt < 0: INT4 output only; gather: slices
+// through pointer tables, INT4 output only); null where there is none.  Each
+// workgroup takes reduce_fixed_tiles(P) groups.
+ReduceKernel reduce_fixed_kernel(int lgB, int P, int ydt, bool gather);
+int reduce_fixed_tiles(int P);
+int reduce_fixed_elems();  // elements per lane of that kernel
 
 }  // namespace zq

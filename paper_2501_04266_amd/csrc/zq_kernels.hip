@@ -478,6 +478,85 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
 // bytes per lane are staged in LDS and written as workgroup-contiguous
 // 16-byte stores, as in the dequantiser.
 
+// One slice into a lane's sum: acc[k] = fl(acc[k] + fl(q_k * s)) for the E
+// codes of the NW words ww (FIRST: acc[k] = fl(q_k * s)).
+template <int E, int NW, bool FIRST>
+__device__ __forceinline__ void add_slice(float (&acc)[E], const uint32_t (&ww)[NW], float sc) {
+  const float s16 = sc * 16.0f;
+  if (__all(s16 <= kMaxFloat)) {  // wave-uniform: 16*s exact for every lane
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float f[8];
+      nibbles_over_16(ww[j], f);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float prod = f[k] * s16;
+        acc[8 * j + k] = FIRST ? prod : acc[8 * j + k] + prod;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NW; ++j) {
+      float f[8];
+      nibbles_over_16(ww[j], f);
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const float prod = (f[k] * 16.0f) * sc;
+        acc[8 * j + k] = FIRST ? prod : acc[8 * j + k] + prod;
+      }
+    }
+  }
+}
+
+// Requantise one wave tile (blocks from blk0, group grp) and store its INT4
+// codes and scales (when out is not null) and, for YDT >= 0, the fused
+// dequantisation fl(code * s_out) in YDT.  ybuf: the workgroup's LDS staging
+// buffer for dequantised outputs wider than 16 bytes per lane; then every
+// wave of the workgroup must call this for the same group.
+template <int B, int E, int YDT>
+__device__ __forceinline__ void requant_tile(const float (&acc)[E], int64_t blk0, int64_t grp, int lane,
+                                             uint8_t* __restrict__ out, float* __restrict__ sout,
+                                             void* __restrict__ y, u32x4* ybuf) {
+  constexpr int L = B / E, NW = E / 8, GB = kThreads / 64 * (64 / L);
+  constexpr int YB = YDT < 0 ? 0 : E * elem_size<(YDT < 0 ? 0 : YDT)>();  // dequantised bytes per lane
+  float a = fabsf(acc[0]);
+#pragma unroll
+  for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
+  const float amax = u2f(group_max<L>(f2u(a)));
+  float so = 0.0f, r = 0.0f;
+  if (amax >= kFlushBelow) {
+    so = scale_of<7>(amax);
+    r = 7.0f / amax;
+  }
+  uint32_t m[E];
+#pragma unroll
+  for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
+  if (out != nullptr) {
+    uint32_t o[NW];
+#pragma unroll
+    for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
+    store_words<ZQ_NT_REDUCE, NW>(out + blk0 * (B / 2) + lane * (E / 2), o);
+    if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk0 + lane / L, so);
+  }
+  if constexpr (YDT >= 0) {
+    // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
+    float v[E];
+#pragma unroll
+    for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
+    if constexpr (YB > 16) {  // every wave of the workgroup is here, at the same group
+      store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
+      __syncthreads();
+      u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + grp * GB * B * elem_size<YDT>());
+#pragma unroll
+      for (int c = 0; c < YB / 16; ++c)
+        st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
+      __syncthreads();
+    } else {
+      store_elems<ZQ_NT_DEQ4, YDT, E>(y, blk0 * B + (int64_t)lane * E, v);
+    }
+  }
+}
+
 template <int U, int NW>
 struct SliceBatch {
   uint32_t w[U][NW];
@@ -530,81 +609,15 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   };
 
   float acc[E];
-  // one slice into the sum, word by word (8 products live at a time)
-  auto accumulate = [&](const uint32_t (&ww)[NW], float sc, bool first) {
-    const float s16 = sc * 16.0f;
-    if (__all(s16 <= kMaxFloat)) {  // wave-uniform: 16*s exact for every lane
-#pragma unroll
-      for (int j = 0; j < NW; ++j) {
-        float f[8];
-        nibbles_over_16(ww[j], f);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const float prod = f[k] * s16;
-          acc[8 * j + k] = first ? prod : acc[8 * j + k] + prod;
-        }
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < NW; ++j) {
-        float f[8];
-        nibbles_over_16(ww[j], f);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          const float prod = (f[k] * 16.0f) * sc;
-          acc[8 * j + k] = first ? prod : acc[8 * j + k] + prod;
-        }
-      }
-    }
-  };
   auto sum_batch = [&](const SliceBatch<U, NW>& X, int b) {
-    if (b == 0) accumulate(X.w[0], X.s[0], true);
-    else accumulate(X.w[0], X.s[0], false);
+    if (b == 0) add_slice<E, NW, true>(acc, X.w[0], X.s[0]);
+    else add_slice<E, NW, false>(acc, X.w[0], X.s[0]);
 #pragma unroll
     for (int u = 1; u < U; ++u)
-      if (b * U + u < P) accumulate(X.w[u], X.s[u], false);
+      if (b * U + u < P) add_slice<E, NW, false>(acc, X.w[u], X.s[u]);
   };
-
   // requantise this wave's tile of group grp and store it
-  auto finish = [&](int64_t grp) {
-    const int64_t blk0 = tile_blk0(grp);
-    float a = fabsf(acc[0]);
-#pragma unroll
-    for (int k = 1; k < E; ++k) a = fmaxf(a, fabsf(acc[k]));
-    const float amax = u2f(group_max<L>(f2u(a)));
-    float so = 0.0f, r = 0.0f;
-    if (amax >= kFlushBelow) {
-      so = scale_of<7>(amax);
-      r = 7.0f / amax;
-    }
-    uint32_t m[E];
-#pragma unroll
-    for (int k = 0; k < E; ++k) m[k] = code_bits(acc[k], r);
-    if (out != nullptr) {
-      uint32_t o[NW];
-#pragma unroll
-      for (int j = 0; j < NW; ++j) o[j] = pack_nibbles8(m + 8 * j);
-      store_words<ZQ_NT_REDUCE, NW>(out + blk0 * (B / 2) + lane_byte, o);
-      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(sout + blk0 + lane / L, so);
-    }
-    if constexpr (YDT >= 0) {
-      // code as float: (1.5*2^23 + q) - 1.5*2^23 = q exactly; then fl(q * s_out)
-      float v[E];
-#pragma unroll
-      for (int k = 0; k < E; ++k) v[k] = (u2f(m[k]) - kRoundMagic) * so;
-      if constexpr (YSTAGE) {  // every wave of the workgroup is here, at the same group
-        store_elems<0, YDT, E>(reinterpret_cast<char*>(ybuf) + threadIdx.x * YB, 0, v);
-        __syncthreads();
-        u32x4* dst = reinterpret_cast<u32x4*>(static_cast<char*>(y) + grp * GB * B * elem_size<YDT>());
-#pragma unroll
-        for (int c = 0; c < YB / 16; ++c)
-          st<ZQ_NT_DEQ4>(dst + c * kThreads + threadIdx.x, ybuf[c * kThreads + threadIdx.x]);
-        __syncthreads();
-      } else {
-        store_elems<ZQ_NT_DEQ4, YDT, E>(y, blk0 * B + (int64_t)lane * E, v);
-      }
-    }
-  };
+  auto finish = [&](int64_t grp) { requant_tile<B, E, YDT>(acc, tile_blk0(grp), grp, lane, out, sout, y, ybuf); };
 
   SliceBatch<U, NW> A;
   if constexpr (!PIPE) {
@@ -649,6 +662,75 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
         next(ct, cb);
       }
     }
+  }
+}
+
+// Vector path with the slice count fixed at compile time (PC = 2, 4 or 8).
+// Same lane layout, arithmetic and order as k_reduce, but every load is
+// unconditional, so the compiler waits for each slice's data on its own
+// (s_waitcnt vmcnt(n) counting the loads issued after it) instead of for
+// every load in flight, and the sum of slice 0 starts while the others are
+// still arriving.  A workgroup takes TRC consecutive groups; with TRC > 1 the
+// loads of a wave's next tile are issued before its current tile is summed,
+// so they arrive while it computes (two register buffers).  The last
+// workgroup clamps its group index to the last group and recomputes it,
+// rewriting identical values, instead of branching around loads.
+#ifndef ZQ_FIXED_WAVES
+#define ZQ_FIXED_WAVES 0
+#endif
+#if ZQ_FIXED_WAVES
+#define ZQ_FIXED_ATTR __attribute__((amdgpu_waves_per_eu(ZQ_FIXED_WAVES)))
+#else
+#define ZQ_FIXED_ATTR
+#endif
+template <int B, int E, int PC, int TRC, int YDT, bool GATHER>
+__global__ void __launch_bounds__(kThreads) ZQ_FIXED_ATTR k_reduce_p(const uint8_t* __restrict__ in, const float* __restrict__ sin,
+                                                       int, int64_t slice_bytes, int64_t slice_scales, int64_t nfull,
+                                                       uint8_t* __restrict__ out, float* __restrict__ sout,
+                                                       void* __restrict__ y) {
+  constexpr int L = B / E, BPW = 64 / L, NW = E / 8, WPG = kThreads / 64, GB = WPG * BPW, NBUF = TRC > 1 ? 2 : 1;
+  static_assert(L >= 1 && L <= 64 && (NW == 1 || NW == 2 || NW == 4) && PC >= 1 && TRC >= 1, "lane layout");
+  constexpr int YB = YDT < 0 ? 0 : E * elem_size<(YDT < 0 ? 0 : YDT)>();
+  __shared__ u32x4 ybuf[YB > 16 ? kThreads * YB / 16 : 1];
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane_byte = lane * (E / 2);
+  const int64_t last = nfull / GB - 1;                  // last group
+  const int64_t g0 = (int64_t)blockIdx.x * TRC;
+  auto group_of = [&](int t) { return g0 + t < last ? g0 + t : last; };
+  auto tile_blk0 = [&](int64_t grp) { return (grp * WPG + wv) * BPW; };
+
+  uint32_t w[NBUF][PC][NW];
+  float sc[NBUF][PC];
+  auto issue = [&](int buf, int64_t grp) {
+    const int64_t blk0 = tile_blk0(grp);
+#pragma unroll
+    for (int p = 0; p < PC; ++p) {
+      const uint8_t* tb;
+      const float* sb;
+      if constexpr (GATHER) {
+        tb = reinterpret_cast<const uint8_t* const*>(in)[p] + blk0 * (B / 2);
+        sb = reinterpret_cast<const float* const*>(sin)[p] + blk0;
+      } else {
+        tb = in + blk0 * (B / 2) + (int64_t)p * slice_bytes;
+        sb = sin + blk0 + (int64_t)p * slice_scales;
+      }
+      load_words<ZQ_NT_REDUCE, NW>(tb + lane_byte, w[buf][p]);
+      sc[buf][p] = ld<ZQ_NT_REDUCE>(sb + lane / L);
+    }
+  };
+
+  issue(0, group_of(0));
+#pragma unroll
+  for (int t = 0; t < TRC; ++t) {
+    if (t + 1 < TRC) issue((t + 1) % NBUF, group_of(t + 1));
+    const int b = t % NBUF;
+    float acc[E];
+    add_slice<E, NW, true>(acc, w[b][0], sc[b][0]);
+#pragma unroll
+    for (int p = 1; p < PC; ++p) add_slice<E, NW, false>(acc, w[b][p], sc[b][p]);
+    const int64_t grp = group_of(t);
+    requant_tile<B, E, YDT>(acc, tile_blk0(grp), grp, lane, out, sout, y, ybuf);
   }
 }
 
@@ -824,6 +906,49 @@ ReduceKernel reduce_gather_kernel(int lgB, ReduceShape shape) {
     default: return &k_reduce<1024, EL, UL, TL, PL, -1, true>;
   }
 #undef ZQ_GATHER_CASE
+}
+
+#ifndef ZQ_FIXED_TR2
+#define ZQ_FIXED_TR2 4
+#endif
+#ifndef ZQ_FIXED_TR4
+#define ZQ_FIXED_TR4 1
+#endif
+#ifndef ZQ_FIXED_TR8
+#define ZQ_FIXED_TR8 1
+#endif
+constexpr int fixed_tiles(int P) { return P == 2 ? ZQ_FIXED_TR2 : P == 4 ? ZQ_FIXED_TR4 : ZQ_FIXED_TR8; }
+int reduce_fixed_tiles(int P) { return fixed_tiles(P); }
+
+#ifndef ZQ_FIXED_E
+#define ZQ_FIXED_E 32
+#endif
+int reduce_fixed_elems() { return ZQ_FIXED_E; }
+
+template <int B, int YDT, bool GATHER>
+static ReduceKernel reduce_fixed_for_b(int P) {
+  constexpr int E = ZQ_FIXED_E;
+  if (P == 2) return &k_reduce_p<B, E, 2, fixed_tiles(2), YDT, GATHER>;
+  if (P == 4) return &k_reduce_p<B, E, 4, fixed_tiles(4), YDT, GATHER>;
+  return &k_reduce_p<B, E, 8, fixed_tiles(8), YDT, GATHER>;
+}
+
+template <int YDT, bool GATHER>
+static ReduceKernel reduce_fixed_for(int lgB, int P) {
+  if (lgB == 6) return reduce_fixed_for_b<64, YDT, GATHER>(P);
+  if (lgB == 7) return reduce_fixed_for_b<128, YDT, GATHER>(P);
+  return reduce_fixed_for_b<256, YDT, GATHER>(P);
+}
+
+ReduceKernel reduce_fixed_kernel(int lgB, int P, int ydt, bool gather) {
+  if (lgB < 6 || lgB > 8 || (P != 2 && P != 4 && P != 8) || (gather && ydt >= 0)) return nullptr;
+  if (gather) return reduce_fixed_for<-1, true>(lgB, P);
+  switch (ydt) {
+    case ZQ_F32: return reduce_fixed_for<ZQ_F32, false>(lgB, P);
+    case ZQ_F16: return reduce_fixed_for<ZQ_F16, false>(lgB, P);
+    case ZQ_BF16: return reduce_fixed_for<ZQ_BF16, false>(lgB, P);
+    default: return reduce_fixed_for<-1, false>(lgB, P);
+  }
 }
 
 ReduceGenericKernel reduce_generic_kernel(bool gather) {

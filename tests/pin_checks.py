@@ -19,6 +19,7 @@ Pins used (none re-types the oracle's own formula):
 """
 import json
 import os
+from fractions import Fraction as Fr
 
 import numpy as np
 
@@ -412,6 +413,156 @@ def check_reduce_invariants(m=1 << 16, seed=9):
 
 
 # --------------------------------------------------------------------------
+# reduce-level edge inputs: sums below the flush threshold, huge scales
+# --------------------------------------------------------------------------
+
+def pack_int4(codes):
+    """Two's-complement nibbles of an int array (last axis), element 2j in the
+    low nibble of byte j; an odd length leaves the last high nibble 0."""
+    c = np.asarray(codes, np.int64)
+    if c.shape[-1] % 2:
+        c = np.concatenate([c, np.zeros(c.shape[:-1] + (1,), np.int64)], axis=-1)
+    nib = c & 0xF
+    return (nib[..., 0::2] | (nib[..., 1::2] << 4)).astype(np.uint8)
+
+
+def special_reduce_slices(kind, P, m, block, seed):
+    """P INT4 slices of m elements (packed bytes [P * ceil(m/2)], scales
+    [P * ceil(m/B)]) that drive a reduce level into its rare cases.
+
+    'subthreshold': scales 2^-128 .. 2^-112 (some binary32 subnormals), one
+      level per block shared by its slices, codes over the whole nibble range
+      -8..7, and every odd slice cancelling most of the slice before it
+      (negated codes, a scale within 1% of its scale; an unpaired last slice
+      is 2^-12 smaller), so that many block sums are non-zero yet below the
+      2^-119 flush threshold, others just above it, and some exactly zero.
+    'huge': slice 0 with scales 2^122 .. 2^125 (binary32 overflows at
+      2^128, so 16 times such a scale is not finite above 2^124) in the
+      first half of the blocks and ordinary scales in the second half; the
+      other slices have scales of 2^-30 .. 2^100, so every product and sum
+      stays finite."""
+    g = _rng(seed)
+    nb = (m + block - 1) // block
+    if kind == "subthreshold":
+        codes = g.integers(-8, 8, (P, m))
+        level = g.uniform(-127, -113, nb)               # shared by the slices of a block
+        scales = np.exp2(level + g.uniform(-1, 1, (P, nb))).astype(np.float32)
+        if P % 2:                                       # the unpaired last slice stays small
+            scales[P - 1] = np.exp2(level - 12).astype(np.float32)
+        for p in range(1, P, 2):
+            keep = g.random(m) < 0.85
+            codes[p] = np.where(keep, -np.clip(codes[p - 1], -7, 7), codes[p])
+            near = (scales[p - 1].astype(np.float64) * (1 + g.uniform(-0.01, 0.01, nb))).astype(np.float32)
+            same = g.random(nb) < 0.25
+            scales[p] = np.where(same, scales[p - 1], near)
+    elif kind == "huge":
+        codes = g.integers(-7, 8, (P, m))
+        scales = np.exp2(g.uniform(-30, 100, (P, nb))).astype(np.float32)
+        big = np.exp2(g.uniform(122, 125, nb)).astype(np.float32)
+        scales[0] = np.where(np.arange(nb) < nb // 2, big, scales[0])
+    else:
+        raise ValueError(kind)
+    return pack_int4(codes).reshape(-1), scales.reshape(-1)
+
+
+def reduce_sums_f32(packed, scales, P, m, block):
+    """The level's binary32 sums, recomputed with numpy's float32 arithmetic
+    (one rounding per multiply and per add, ascending slice order).  Used
+    only to confirm that an edge-case input really reaches the case it is
+    built for, never as an expected value."""
+    pk = np.asarray(packed, np.uint8).reshape(P, -1)
+    sc = np.asarray(scales, np.float32).reshape(P, -1)
+    nib = np.empty((P, 2 * pk.shape[1]), np.int64)
+    nib[:, 0::2], nib[:, 1::2] = pk & 0xF, pk >> 4
+    q = np.where(nib >= 8, nib - 16, nib)[:, :m].astype(np.float32)
+    s = np.repeat(sc, block, axis=1)[:, :m]
+    acc = np.zeros(m, np.float32)
+    with np.errstate(over="raise"):
+        for p in range(P):
+            acc = acc + q[p] * s[p]
+    return acc
+
+
+def subthreshold_block_counts(packed, scales, P, m, block):
+    """(blocks whose sum is non-zero but below 2^-119, blocks at or above it)."""
+    acc = np.abs(reduce_sums_f32(packed, scales, P, m, block).astype(np.float64))
+    nb = (m + block - 1) // block
+    pad = np.zeros(nb * block)
+    pad[:m] = acc
+    amax = pad.reshape(nb, block).max(axis=1)
+    return int(np.count_nonzero((amax > 0) & (amax < 2.0 ** -119))), int(np.count_nonzero(amax >= 2.0 ** -119))
+
+
+def check_brute_special_reduce():
+    """The oracle's reduce level on sums below the flush threshold (incl.
+    subnormal products) and on scales near the top of the binary32 range,
+    against brute force."""
+    for kind, P, m, block, seed in (("subthreshold", 2, 256, 32, 70), ("subthreshold", 3, 200, 64, 71),
+                                    ("huge", 1, 96, 32, 72), ("huge", 2, 256, 64, 73)):
+        pin, sin = special_reduce_slices(kind, P, m, block, seed)
+        if kind == "subthreshold":
+            low, high = subthreshold_block_counts(pin, sin, P, m, block)
+            assert low > 0 and high > 0, "edge input misses the flush threshold"
+        nb = (m + block - 1) // block
+        pk = pin.reshape(P, -1)
+        sl = [(brute.unpack_int4(pk[p], m), [Fr(float(v)) for v in sin[p * nb:(p + 1) * nb]]) for p in range(P)]
+        bc, bs = brute.reduce_level(sl, block)
+        op, os_ = oracle.qgz_reduce_level(pin, sin, P, m, block)
+        assert brute.unpack_int4(op, m) == bc, f"reduce codes differ ({kind} P={P} m={m} B={block})"
+        assert [int(v) for v in os_.view(np.uint32)] == [brute.to_f32_bits(s) for s in bs], \
+            f"reduce scales differ ({kind} P={P} m={m} B={block})"
+
+
+# --------------------------------------------------------------------------
+# the multi-level chain
+# --------------------------------------------------------------------------
+
+CHAIN_CASES = [
+    # (n, fan-ins, rank, block, seed)
+    (2304, (3, 4, 3), 2, 32, 80),
+    (3072, (2, 4, 3), 1, 64, 81),
+]
+
+
+def check_brute_chain(chain_fn=None, cases=CHAIN_CASES):
+    """oracle.chain against a brute-force composition of the levels: the own
+    gradient quantised, then per level the own chunk `rank` of the previous
+    output (codes and scales cut at the same element offset) with seeded peer
+    slices, reduced in exact arithmetic.  A non-zero rank exercises the chunk
+    offsets."""
+    chain_fn = chain_fn or oracle.chain
+    for n, fanins, rank, block, seed in cases:
+        g = _rng(seed)
+        own = (g.standard_normal(n) * 1e-3).astype(np.float32)
+        cur_c, cur_s = brute.quantize(brute.exact_values(own, "f32"), block, 7)
+        op_, os_ = oracle.qgz_quantize(own, block)
+        want, peers, cur_m = [], [], n
+        for P in fanins:
+            m = cur_m // P
+            nbm = m // block
+            slices, lvl = [], []
+            for p in range(P):
+                if p == rank:
+                    slices.append((cur_c[rank * m:(rank + 1) * m], cur_s[rank * nbm:(rank + 1) * nbm]))
+                    lvl.append(None)
+                else:
+                    x = (g.standard_normal(m) * 10.0 ** g.uniform(-4, 0)).astype(np.float32)
+                    slices.append(brute.quantize(brute.exact_values(x, "f32"), block, 7))
+                    lvl.append(oracle.qgz_quantize(x, block))
+            cur_c, cur_s = brute.reduce_level(slices, block)
+            want.append((m, cur_c, cur_s))
+            peers.append(lvl)
+            cur_m = m
+        outs = chain_fn(op_, os_, n, list(fanins), peers, rank, block)
+        assert len(outs) == len(fanins), "chain: wrong number of levels"
+        for k, ((m, bc, bs), (gp, gs, gm)) in enumerate(zip(want, outs)):
+            assert gm == m, f"chain level {k}: size {gm}, want {m}"
+            assert brute.unpack_int4(gp, m) == bc, f"chain level {k} codes differ (rank {rank})"
+            assert [int(v) for v in np.asarray(gs, np.float32).view(np.uint32)] == [brute.to_f32_bits(s) for s in bs], \
+                f"chain level {k} scales differ (rank {rank})"
+
+
+# --------------------------------------------------------------------------
 # element formats against library conversions
 # --------------------------------------------------------------------------
 
@@ -472,6 +623,8 @@ ALL = [
     ("brute_reduce", lambda: [check_brute_reduce(*c) for c in BRUTE_REDUCE_CASES]),
     ("invariants", lambda: check_invariants(n=1 << 18)),
     ("reduce_invariants", lambda: check_reduce_invariants(m=1 << 14)),
+    ("brute_special_reduce", check_brute_special_reduce),
+    ("brute_chain", check_brute_chain),
     ("formats", check_format_conversions),
 ]
 

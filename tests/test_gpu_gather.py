@@ -74,3 +74,29 @@ def test_gather_from_views_and_graph_replay():
         torch.cuda.synchronize()
         assert_bits_equal(from_dev(gp), op, f"replay {rep} packed", block // 2)
         assert_bits_equal(from_dev(gs), os_, f"replay {rep} scales")
+
+
+def test_gather_binding_checks_and_raw_stream():
+    """The binding rejects byte slices that are not 16-byte aligned where the
+    vector path needs them (the library cannot read device-resident
+    addresses), and a call on a raw stream handle keeps the tables it built
+    alive until the kernel has run."""
+    P, block, m = 3, 128, 1 << 16
+    sl = _slices(P, m, block, 91)
+    packed = [to_dev(a) for a, _ in sl]
+    scales = [to_dev(b) for _, b in sl]
+    big = torch.zeros(m // 2 + 16, dtype=torch.uint8, device="cuda")
+    shifted = big[1:1 + m // 2]
+    shifted.copy_(packed[1])
+    with pytest.raises(ValueError):
+        zq.qgz_reduce_level_gather([packed[0], shifted, packed[2]], scales, m, block)
+    op, os_ = oracle.qgz_reduce_level(np.concatenate([a for a, _ in sl]), np.concatenate([b for _, b in sl]),
+                                      P, m, block)
+    gp, gs = poisoned(m // 2, torch.uint8), poisoned(m // block, torch.float32)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())      # the inputs' uploads and the poison fill
+    for _ in range(3):
+        zq.qgz_reduce_level_gather(packed, scales, m, block, packed_out=gp, scales_out=gs, stream=s.cuda_stream)
+    s.synchronize()
+    assert_bits_equal(from_dev(gp), op, "raw-stream gather packed", block // 2)
+    assert_bits_equal(from_dev(gs), os_, "raw-stream gather scales")

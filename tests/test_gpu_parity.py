@@ -420,3 +420,58 @@ def test_concurrent_host_threads_on_separate_streams():
         assert_bits_equal(p, want[i][0], f"thread {i} packed", block // 2)
         assert_bits_equal(sc, want[i][1], f"thread {i} scales")
         assert_bits_equal(y, oracle.qgz_dequantize(want[i][0], want[i][1], n, block, "f32"), f"thread {i} dequant")
+
+
+# Inputs that reach the reduce level's rare branches (tests/pin_checks.py,
+# special_reduce_slices): non-zero block sums below the 2^-119 flush
+# threshold (with subnormal products), and slice scales above 2^124, for
+# which 16 * s is not finite.  Each on the large (P >= 3), two-slice
+# (P <= 2) and small-level vector shapes and on the per-block generic kernel
+# (ragged m, and the leftover blocks after the last whole group).
+SPECIAL_REDUCE_CASES = [
+    ("subthreshold", 2, 128, (1 << 23) + 4096),
+    ("subthreshold", 3, 128, (1 << 23) + 4096),
+    ("subthreshold", 8, 128, 65536 + 128),
+    ("subthreshold", 48, 64, 16384),
+    ("subthreshold", 5, 64, 4095),
+    ("subthreshold", 2, 1024, 16 * 1024 + 32),
+    ("huge", 1, 128, (1 << 23) + 4096),
+    ("huge", 2, 128, (1 << 23) + 4096),
+    ("huge", 3, 128, (1 << 23) + 4096),
+    ("huge", 3, 256, 65536 + 256),
+    ("huge", 2, 64, 1000),
+]
+
+
+@pytest.mark.parametrize("kind,P,block,m", SPECIAL_REDUCE_CASES)
+def test_reduce_edge_sums(kind, P, block, m):
+    """The reduce level, the fused last level and the gathered-slice form on
+    edge sums, bit for bit against the oracle."""
+    what = f"{kind} P={P} B={block} m={m}"
+    pin, sin = pc.special_reduce_slices(kind, P, m, block, 7 * P + m + block)
+    nb, mb = zq.num_scales(m, block), zq.int4_bytes(m)
+    if kind == "subthreshold":
+        low, high = pc.subthreshold_block_counts(pin, sin, P, m, block)
+        assert low > 0 and high > 0, f"{what}: input misses the flush threshold"
+    else:
+        assert float(sin[:nb].max()) > 2.0 ** 124, f"{what}: no scale above 2^124"
+    po, so = oracle.qgz_reduce_level(pin, sin, P, m, block)
+    dpin, dsin = to_dev(pin), to_dev(sin)
+    gp, gs = zq.qgz_reduce_level(dpin, dsin, P, m, block)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(gp), po, f"{what} packed", block // 2)
+    assert_bits_equal(from_dev(gs), so, f"{what} scales")
+    for out, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        want = oracle.qgz_dequantize(po, so, m, block, out)
+        fp, fs = poisoned(mb, torch.uint8), poisoned(nb, torch.float32)
+        y = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt, packed_out=fp, scales_out=fs)
+        torch.cuda.synchronize()
+        assert_bits_equal(from_dev(y), want, f"{what} fused -> {out}")
+        assert_bits_equal(from_dev(fp), po, f"{what} fused INT4 packed", block // 2)
+        assert_bits_equal(from_dev(fs), so, f"{what} fused INT4 scales")
+    ps = [dpin[p * mb:(p + 1) * mb].clone() for p in range(P)]
+    ss = [dsin[p * nb:(p + 1) * nb].clone() for p in range(P)]
+    hp, hs = zq.qgz_reduce_level_gather(ps, ss, m, block)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(hp), po, f"{what} gather packed", block // 2)
+    assert_bits_equal(from_dev(hs), so, f"{what} gather scales")

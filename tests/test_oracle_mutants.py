@@ -77,3 +77,54 @@ def test_every_mutant_is_caught():
             results = list(ex.map(lambda m: _mutant(tmp, *m), MUTANTS))
     survivors = [name for name, failed in results if not failed]
     assert not survivors, f"mutants not caught by any pin: {survivors}"
+
+
+# Mistakes planted in the oracle's level composition (oracle.chain), which is
+# Python: each is applied to the function's source and the brute-force chain
+# pin must reject the result (a crash also counts as detection; every mutant
+# here keeps the slice sizes right, except the stale level size).
+CHAIN_MUTANTS = [
+    ("own-chunk-always-0", [("own_chunk_p = cur_p[rank * mb:(rank + 1) * mb]", "own_chunk_p = cur_p[0:mb]"),
+                            ("own_chunk_s = cur_s[rank * nbm:(rank + 1) * nbm]", "own_chunk_s = cur_s[0:nbm]")]),
+    ("scale-offset-in-chunks", [("own_chunk_s = cur_s[rank * nbm:(rank + 1) * nbm]",
+                                 "own_chunk_s = cur_s[rank:rank + nbm]")]),
+    ("next-chunk", [("own_chunk_p = cur_p[rank * mb:(rank + 1) * mb]",
+                     "own_chunk_p = cur_p[(rank + 1) % P * mb:((rank + 1) % P + 1) * mb]"),
+                    ("own_chunk_s = cur_s[rank * nbm:(rank + 1) * nbm]",
+                     "own_chunk_s = cur_s[(rank + 1) % P * nbm:((rank + 1) % P + 1) * nbm]")]),
+    ("own-slice-first", [("for p in range(P):\n            if p == rank:",
+                          "slices_p.append(own_chunk_p)\n        slices_s.append(own_chunk_s)\n"
+                          "        for p in range(P):\n            if p == rank:\n                continue\n"
+                          "            if False:")]),
+    ("stale-level-size", [("        cur_m = m\n", "")]),
+]
+
+
+def _mutated_chain(subs):
+    import inspect
+    import textwrap
+
+    import numpy as np
+
+    import oracle
+    src = textwrap.dedent(inspect.getsource(oracle.chain))
+    for old, new in subs:
+        assert src.count(old) == 1, f"chain mutant pattern not found: {old}"
+        src = src.replace(old, new)
+    ns = {"np": np, "num_scales": oracle.num_scales, "int4_bytes": oracle.int4_bytes,
+          "qgz_reduce_level": oracle.qgz_reduce_level}
+    exec(compile(src, "<chain mutant>", "exec"), ns)
+    return ns["chain"]
+
+
+def test_chain_passes_pin():
+    from tests import pin_checks
+    pin_checks.check_brute_chain()
+
+
+@pytest.mark.parametrize("name,subs", CHAIN_MUTANTS, ids=[m[0] for m in CHAIN_MUTANTS])
+def test_every_chain_mutant_is_caught(name, subs):
+    from tests import pin_checks
+    fn = _mutated_chain(subs)
+    with pytest.raises(Exception):
+        pin_checks.check_brute_chain(chain_fn=fn)
