@@ -146,6 +146,29 @@ int qgz_reduce_dequantize(const uint8_t* packed_in, const float* scales_in, int3
 int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P,
                             int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream);
 
+/* Allocation-free form of qgz_reduce_level_gather, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  The P slice addresses come in HOST
+ * arrays; the library writes them into a static device table of its own (one
+ * per GPU, 2048 addresses = 16 KiB, held until the process ends) with small
+ * kernels on `stream` whose values travel as kernel arguments, then runs the
+ * gathered reduce over them.  Nothing is allocated and nothing synchronises.
+ *   packed_slices  host array of P device pointers; slice p holds ceil(m/2) bytes
+ *   scale_slices   host array of P device pointers; slice p holds ceil(m/block) floats
+ *   packed_out, scales_out as qgz_reduce_level (both required)
+ * The host arrays are read before the call returns.  1 <= P <= 1024 (larger P
+ * is ZQ_E_P: the table holds 1024 pairs).  Because the addresses are on the
+ * host, every slice is checked: non-null (ZQ_E_NULL), 16-byte aligned when
+ * m % 32 == 0 and scale slices 4-byte aligned (ZQ_E_ALIGN), no overlap with
+ * an output (ZQ_E_ALIAS).  The table belongs to the current device, and
+ * `stream` must belong to it too.  Every call on one GPU uses the same table:
+ * calls that can overlap on one GPU (different streams, or different host
+ * threads without ordering) race on it; calls on one stream are ordered.
+ * Results are bit-identical to qgz_reduce_level_gather (and qgz_reduce_level
+ * on the slices back to back). */
+int qgz_reduce_level_gather_noalloc(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P,
+                                    int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream);
+
 /* Dequantise-on-load GEMM: the forward product of a layer whose weight
  * arrives as the gathered INT8 buffer (Design, Weight Partitioning: the
  * Allgathered weights are dequantised for the forward pass), without writing

@@ -19,6 +19,7 @@ from ._lib import (  # noqa: F401
     qgz_reduce_dequantize,
     qgz_reduce_level,
     qgz_reduce_level_gather,
+    qgz_reduce_level_gather_noalloc,
     qwz_dequant_gemm,
     qwz_dequantize,
     qwz_quantize,

@@ -17,8 +17,8 @@ ZQ_F32, ZQ_F16, ZQ_BF16 = 0, 1, 2
 STATUS = {0: "ZQ_OK", -1: "ZQ_E_NULL", -2: "ZQ_E_BLOCK", -3: "ZQ_E_DTYPE", -4: "ZQ_E_ALIGN",
           -5: "ZQ_E_SIZE", -6: "ZQ_E_P", -7: "ZQ_E_HIP", -8: "ZQ_E_ALIAS"}
 EXPORTS = ["qwz_quantize", "qwz_dequantize", "qgz_quantize", "qgz_reduce_level", "qgz_dequantize",
-           "qgz_reduce_dequantize", "qgz_reduce_level_gather", "qwz_dequant_gemm", "zq_num_scales",
-           "zq_int4_bytes", "zq_status_string"]
+           "qgz_reduce_dequantize", "qgz_reduce_level_gather", "qgz_reduce_level_gather_noalloc",
+           "qwz_dequant_gemm", "zq_num_scales", "zq_int4_bytes", "zq_status_string"]
 
 _TORCH_DT = {torch.float32: ZQ_F32, torch.float16: ZQ_F16, torch.bfloat16: ZQ_BF16}
 _DT_TORCH = {v: k for k, v in _TORCH_DT.items()}
@@ -49,6 +49,7 @@ def lib():
         "qgz_reduce_dequantize": [vp, vp, i32, i64, i32, vp, ci, vp, vp, vp],
         "qwz_dequant_gemm": [vp, ci, vp, vp, i64, i64, i64, i32, vp, vp],
         "qgz_reduce_level_gather": [vp, vp, i32, i64, i32, vp, vp, vp],
+        "qgz_reduce_level_gather_noalloc": [vp, vp, i32, i64, i32, vp, vp, vp],
     }
     for name, args in sig.items():
         fn = getattr(L, name)
@@ -264,6 +265,29 @@ def qgz_reduce_level_gather(packed_slices, scale_slices, m, block=128, packed_ou
     _check(lib().qgz_reduce_level_gather(tab.data_ptr(), stab.data_ptr(), P, m, block,
                                          _dev(packed_out, "packed_out"), _dev(scales_out, "scales_out"),
                                          _stream(stream)), "qgz_reduce_level_gather")
+    return packed_out, scales_out
+
+
+def qgz_reduce_level_gather_noalloc(packed_slices, scale_slices, m, block, packed_out, scales_out, stream=None):
+    """qgz_reduce_level_gather without any device allocation: the slice
+    addresses go to the library in host arrays (it keeps its own device table
+    per GPU), and the caller passes the outputs.  Calls that may overlap on
+    one GPU share that table and must be ordered (one stream)."""
+    import ctypes
+    P = len(packed_slices)
+    if P != len(scale_slices) or P == 0:
+        raise ValueError("give P >= 1 byte slices and as many scale slices")
+    for p, (a, b) in enumerate(zip(packed_slices, scale_slices)):
+        _need(a, f"packed_slices[{p}]", int4_bytes(m), _U8)
+        _need(b, f"scale_slices[{p}]", _nsc(m, block), _F32)
+    _need(packed_out, "packed_out", int4_bytes(m), _U8)
+    _need(scales_out, "scales_out", _nsc(m, block), _F32)
+    tab = (ctypes.c_void_p * P)(*[_dev(t, f"packed_slices[{p}]") for p, t in enumerate(packed_slices)])
+    stab = (ctypes.c_void_p * P)(*[_dev(t, f"scale_slices[{p}]") for p, t in enumerate(scale_slices)])
+    _check(lib().qgz_reduce_level_gather_noalloc(ctypes.cast(tab, ctypes.c_void_p), ctypes.cast(stab, ctypes.c_void_p),
+                                                 P, m, block, _dev(packed_out, "packed_out"),
+                                                 _dev(scales_out, "scales_out"), _stream(stream)),
+           "qgz_reduce_level_gather_noalloc")
     return packed_out, scales_out
 
 

@@ -8,6 +8,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "zq.h"
 #include "zq_host.h"
 #include "zq_internal.h"
@@ -158,6 +160,73 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
   return ZQ_OK;
 }
 
+// Slice-address tables of qgz_reduce_level_gather_noalloc: one static array
+// per GPU, held until the process ends (packed-slice addresses in entries
+// [0, P), scale-slice addresses in [P, 2P)).  Host code never uses this name
+// as an address: the device address comes from hipGetSymbolAddress, once per
+// device (scratch_on_current_device).
+constexpr int kScratchEntries = 2 * 1024;
+constexpr int kMaxDevices = 64;
+static __device__ __align__(256) uint64_t scratch[kScratchEntries];
+
+// Device address of `scratch` on the current device (looked up on the
+// first call on each device, with that device current); ZQ_E_HIP if HIP
+// cannot give it.
+int scratch_on_current_device(uint64_t** out) {
+  static std::once_flag once[kMaxDevices];
+  static uint64_t* addr[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return ZQ_E_HIP;
+  std::call_once(once[dev], [dev] {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) == hipSuccess) addr[dev] = static_cast<uint64_t*>(p);
+  });
+  if (addr[dev] == nullptr) return ZQ_E_HIP;
+  *out = addr[dev];
+  return ZQ_OK;
+}
+
+// The reduce level over slices whose addresses are in host arrays: the
+// addresses are checked on the host, written into this device's scratch
+// table by fill kernels on the stream (their values travel as kernel
+// arguments), and the gathered reduce reads them from there.
+int reduce_gather_host(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P, int64_t m,
+                       int32_t block, uint8_t* packed_out, float* scales_out, void* stream) {
+  if (m < 0) return ZQ_E_SIZE;
+  if (log2_block(block) < 0) return ZQ_E_BLOCK;
+  if (P < 1 || 2 * (int64_t)P > kScratchEntries) return ZQ_E_P;
+  if (m == 0) return ZQ_OK;
+  if (!packed_slices || !scale_slices || !packed_out || !scales_out) return ZQ_E_NULL;
+  const int64_t slice_bytes = (m + 1) / 2, nb = num_scales(m, block);
+  const Range outs[] = {{packed_out, slice_bytes}, {scales_out, 4 * nb}};
+  for (int32_t p = 0; p < P; ++p) {
+    if (!packed_slices[p] || !scale_slices[p]) return ZQ_E_NULL;
+    if ((m % 32 == 0 && !aligned(packed_slices[p], 16)) || !aligned(scale_slices[p], 4)) return ZQ_E_ALIGN;
+    const Range ins[] = {{packed_slices[p], slice_bytes}, {scale_slices[p], 4 * nb}};
+    for (const Range& o : outs)
+      for (const Range& i : ins)
+        if (overlap(o, i)) return ZQ_E_ALIAS;
+  }
+  uint64_t* table = nullptr;
+  int rc = scratch_on_current_device(&table);
+  if (rc != ZQ_OK) return rc;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int64_t entries = 2 * (int64_t)P;
+  for (int64_t e0 = 0; e0 < entries; e0 += kTableChunk) {
+    TableChunk chunk;
+    const int count = (int)(entries - e0 < kTableChunk ? entries - e0 : kTableChunk);
+    for (int k = 0; k < count; ++k) {
+      const int64_t e = e0 + k;
+      chunk.v[k] = e < P ? reinterpret_cast<uint64_t>(packed_slices[e]) : reinterpret_cast<uint64_t>(scale_slices[e - P]);
+    }
+    for (int k = count; k < kTableChunk; ++k) chunk.v[k] = 0;
+    rc = launch(fill_table_kernel(), 1u, (unsigned)kTableChunk, st, table + e0, chunk, count);
+    if (rc != ZQ_OK) return rc;
+  }
+  return reduce(reinterpret_cast<const uint8_t*>(table), reinterpret_cast<const float*>(table + P), P, m, block,
+                packed_out, scales_out, false, nullptr, -1, stream, true);
+}
+
 }  // namespace
 
 extern "C" {
@@ -196,6 +265,11 @@ int qgz_reduce_level_gather(const uint8_t* const* packed_slices, const float* co
                             int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream) {
   return reduce(reinterpret_cast<const uint8_t*>(packed_slices), reinterpret_cast<const float*>(scale_slices), P, m,
                 block, packed_out, scales_out, false, nullptr, -1, stream, true);
+}
+
+int qgz_reduce_level_gather_noalloc(const uint8_t* const* packed_slices, const float* const* scale_slices, int32_t P,
+                                    int64_t m, int32_t block, uint8_t* packed_out, float* scales_out, void* stream) {
+  return reduce_gather_host(packed_slices, scale_slices, P, m, block, packed_out, scales_out, stream);
 }
 
 int64_t zq_num_scales(int64_t n, int32_t block) {

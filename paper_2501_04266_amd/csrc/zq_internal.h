@@ -98,6 +98,13 @@ ReduceGenericKernel reduce_generic_kernel(bool gather);
 // through pointer tables, INT4 output only); null where there is none.  Each
 // workgroup takes reduce_fixed_tiles(P) groups.
 ReduceKernel reduce_fixed_kernel(int lgB, int P, int ydt, bool gather);
+// a chunk of 64-bit table entries passed by value to the table-fill kernel
+constexpr int kTableChunk = 64;
+struct TableChunk {
+  uint64_t v[kTableChunk];
+};
+using FillTableKernel = void (*)(uint64_t*, TableChunk, int);
+FillTableKernel fill_table_kernel();
 int reduce_fixed_tiles(int P);
 int reduce_fixed_elems();  // elements per lane of that kernel
 

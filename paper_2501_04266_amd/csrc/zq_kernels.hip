@@ -806,6 +806,16 @@ __global__ void __launch_bounds__(64) k_reduce_generic(const uint8_t* __restrict
   if (lane == 0 && out != nullptr) sout[blk] = so;
 }
 
+// ------------------------------------------------------------------ address tables
+// Writes count (<= kTableChunk) 64-bit entries carried in the kernel
+// arguments to dst[0, count): lane t stores entry t with a vector store.
+__global__ void __launch_bounds__(kTableChunk) k_fill_table(uint64_t* __restrict__ dst, TableChunk chunk, int count) {
+  const int t = threadIdx.x;
+  if (t < count) dst[t] = chunk.v[t];
+}
+
+FillTableKernel fill_table_kernel() { return &k_fill_table; }
+
 // ------------------------------------------------------------------ instantiation tables
 
 template <int DT, int QB>

@@ -199,3 +199,35 @@ def test_reduce_gather_argument_errors(L):
     assert f(vp(T + 4), vp(S), 8, 256, 128, vp(B), vp(B + 4096), None) == -4   # table not 8-byte aligned
     assert f(vp(T), vp(S), 8, 256, 128, vp(T + 32), vp(B + 4096), None) == -8  # output over the table
     assert f(vp(T), vp(S), 8, 0, 128, None, None, None) == 0
+
+
+def test_reduce_gather_noalloc_argument_errors(L):
+    """Every check of the allocation-free gathered reduce runs on the host
+    arrays of slice addresses before anything is enqueued."""
+    f = L.qgz_reduce_level_gather_noalloc
+    vp = ctypes.c_void_p
+    P, m, block = 4, 4096, 128
+    base = 0x7F0050000000
+
+    def tabs(packed, scales):
+        return (ctypes.c_void_p * len(packed))(*packed), (ctypes.c_void_p * len(scales))(*scales)
+
+    pk = [base + p * 0x10000 for p in range(P)]
+    sc = [base + 0x100000 + p * 0x1000 for p in range(P)]
+    out, sout = base + 0x200000, base + 0x300000
+    tp, ts = tabs(pk, sc)
+    assert f(tp, ts, 0, m, block, vp(out), vp(sout), None) == -6
+    assert f(tp, ts, 1025, m, block, vp(out), vp(sout), None) == -6          # beyond the 1024-pair table
+    assert f(tp, ts, P, m, 100, vp(out), vp(sout), None) == -2
+    assert f(tp, ts, P, -1, block, vp(out), vp(sout), None) == -5
+    assert f(None, ts, P, m, block, vp(out), vp(sout), None) == -1
+    assert f(tp, ts, P, m, block, None, vp(sout), None) == -1
+    tq, tt = tabs(pk[:2] + [0] + pk[3:], sc)
+    assert f(tq, tt, P, m, block, vp(out), vp(sout), None) == -1             # a null slice
+    tq, tt = tabs(pk[:2] + [pk[2] + 8] + pk[3:], sc)
+    assert f(tq, tt, P, m, block, vp(out), vp(sout), None) == -4             # slice not 16-byte aligned (m % 32 == 0)
+    tq, tt = tabs(pk, sc[:1] + [sc[1] + 2] + sc[2:])
+    assert f(tq, tt, P, m, block, vp(out), vp(sout), None) == -4             # scale slice not 4-byte aligned
+    assert f(tp, ts, P, m, block, vp(pk[3] + 16), vp(sout), None) == -8     # output over a slice
+    assert f(tp, ts, P, m, block, vp(out), vp(sc[0]), None) == -8           # scales over a scale slice
+    assert f(tp, ts, P, 0, block, None, None, None) == 0
