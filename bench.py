@@ -19,19 +19,33 @@ all-to-all of each level) are outside this path: their results are placed
 in HBM before timing (peer slices are quantised from seeded fp32 peer
 gradients; a level's local slice is chunk 0 of the previous level's output).
 
-Timing: W warm-up steps; a breakdown pass of K steps with HIP events between
-all calls (per-call figures, the `kernels` list); then the timed region of K
-steps, host wall clock between two device synchronisations, with one event
-pair around the dominant kernel only (its per-launch duration gives the
-roofline figure).  Events between launches cost GPU time, so the step time
-is never taken from the breakdown pass.
+Timing of the step: W warm-up steps; a breakdown pass of K steps with HIP
+events between all calls (the per-call event figures); then --settle more
+steps, because the GPU's clock drops for some tens of milliseconds once
+continuous heavy work starts (measured: 2.15 -> 1.57 -> 2.2 GHz over ~60
+launches of the reduce level, and the step from 0.84 to a steady 0.75 ms
+over its first ~40 steps; the breakdown pass's events leave idle gaps that
+let the clock rise again); then the timed region of K steps, host wall clock
+between two device synchronisations, with one event pair around the
+dominant kernel only (its per-launch duration gives the roofline figure).
+The settle steps' times are reported too.
+
+Per-call figures (`kernels`): each call of the step launched back to back in
+a loop, its inputs rotating over copies totalling >= 1 GB so the 256 MB
+last-level cache cannot serve them (loop time / launches, which includes
+the GPU's gap between dependent launches); beside it the call's time inside
+the step's breakdown pass (event brackets), and the kernel-only duration
+from the committed rocprofv3 trace when that was taken on these sources.
 
 Output: one JSON line.  value = algorithmic bytes of the step / step time.
-Extra fields, measured after the timed region: the last level fused with the
-final dequantisation, the degree-2 weight shard, the P = 8 level in
-all-shares mode (m = n) and reading its slices in place from separate
-buffers, and the layer's forward GEMMs with the INT8 weight
-dequantised on load (8192 tokens) against dequantise + torch's GEMM.
+Extra fields, measured after the timed region: the other workloads
+(tiny-1024x1024, gpt-1.3b-layer, outlier-edge-123456789) call by call; the
+bandwidth ceilings of hand-written copy / read / write / P-stream kernels
+(libzq_probe.so); the last level fused with the final dequantisation, the
+degree-2 weight shard, the P = 8 level in all-shares mode (m = n) and
+reading its slices in place from separate buffers, and the layer's forward
+GEMMs with the INT8 weight dequantised on load against dequantise + torch's
+GEMM.
 """
 import argparse
 import json
@@ -47,7 +61,6 @@ METRIC = "achieved HBM GB/s (% of MI355X peak) for qwZ quant/dequant + qgZ reduc
 HBM_PEAK_GBPS = 8000.0
 WBLOCK, GBLOCK, SHARD = 256, 128, 8
 FANINS = [2, 4, 48]
-COPY_REPS = 20
 
 
 def nsc(n, b):
@@ -436,16 +449,313 @@ def cpu_model():
     return "unknown"
 
 
+ROT_BYTES = 1100 * 1000 * 1000   # inputs + outputs rotated per call loop: beyond the 256 MB last-level cache
+GATE_BYTES = 100 * 1000 * 1000   # calls of at least this many bytes are held to 70% of HBM peak
+ALL_SHARES_SETTLE_S = 0.1
+TRACE_PROFILE = os.path.join(ROOT, "profiles", "gpt20b_step_kernel_trace.txt")
+
+
+def _tensor_bytes(ts):
+    return sum(t.numel() * t.element_size() for t in ts)
+
+
+def rotation_runs(fn, inputs, outputs, footprint=None):
+    """Closures running fn(inputs, outputs) over enough copies of the inputs
+    (and separate outputs) that one pass over them moves >= ROT_BYTES: a loop
+    over them streams from HBM, not from the last-level cache.  Copy 0 is the
+    given buffers."""
+    import torch
+    fp = footprint or _tensor_bytes(inputs) + _tensor_bytes(outputs)
+    nsets = max(1, -(-ROT_BYTES // max(1, fp)))
+    runs = [lambda: fn(inputs, outputs)]
+    for _ in range(1, nsets):
+        ins = [t.clone() for t in inputs]
+        outs = [torch.empty_like(t) for t in outputs]
+        runs.append(lambda ins=ins, outs=outs: fn(ins, outs))
+    return runs
+
+
+def loop_us(runs, reps, warm=3):
+    """Mean microseconds per launch over `reps` back-to-back launches cycling
+    through `runs` (events around the whole loop only)."""
+    import torch
+    for i in range(warm):
+        runs[i % len(runs)]()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(reps):
+        runs[i % len(runs)]()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def call_figures(name, nbytes, elems, us, nsets=None):
+    r = {"call": name, "bytes": nbytes, "elements": elems, "us": round(us, 2),
+         "GBps": round(nbytes / (us * 1e-6) / 1e9, 1), "Gelem_per_s": round(elems / (us * 1e-6) / 1e9, 1),
+         "pct_hbm_peak": round(100 * nbytes / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 1)}
+    if nsets is not None:
+        r["rotated_sets"] = nsets
+    return r
+
+
+def timed_calls(specs, reps):
+    """specs: (name, bytes, elements, fn, inputs, outputs) -> per-call figures
+    from rotated back-to-back loops."""
+    import torch
+    out = []
+    for name, nbytes, elems, fn, ins, outs in specs:
+        runs = rotation_runs(fn, ins, outs)
+        us = loop_us(runs, max(reps, 2 * len(runs)))
+        out.append(call_figures(name, nbytes, elems, us, len(runs)))
+        del runs
+        torch.cuda.empty_cache()
+    return out
+
+
+def load_trace(call):
+    """Kernel-only microseconds per launch of `call` in the step, from the
+    committed rocprofv3 kernel trace, or None when there is none or it was
+    taken on different kernel sources."""
+    if not os.path.exists(TRACE_PROFILE):
+        return None
+    lines = open(TRACE_PROFILE).read().splitlines()
+    tag = "# kernel source sha256[:16]:"
+    h = next((ln[len(tag):].strip() for ln in lines if ln.startswith(tag)), None)
+    if h != kernel_source_hash():
+        return None
+    for ln in lines:
+        if ln.startswith(call + "  ") and not ln.startswith("#"):
+            rest = ln[len(call):].split()
+            return float(rest[-4])
+    return None
+
+
+class Probe:
+    """The bandwidth-ceiling kernels of libzq_probe.so (copy, read, write,
+    P read streams + one write stream)."""
+
+    def __init__(self):
+        import ctypes
+
+        import torch
+        from paper_2501_04266_amd import build as zbuild
+        if not os.path.exists(zbuild.PROBE_LIB):
+            raise ImportError(f"{zbuild.PROBE_LIB} is not built; run `python -m paper_2501_04266_amd.build`")
+        L = ctypes.CDLL(zbuild.PROBE_LIB)
+        vp, i64, i32, u32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32
+        for name, args in {"zqp_copy": [vp, vp, i64, vp], "zqp_read": [vp, i64, vp, u32, vp],
+                           "zqp_write": [vp, i64, u32, vp], "zqp_streams": [vp, i32, i64, vp, vp]}.items():
+            getattr(L, name).argtypes, getattr(L, name).restype = args, ctypes.c_int
+        self.L, self.torch = L, torch
+
+    def _st(self):
+        return self.torch.cuda.current_stream().cuda_stream
+
+    def _ok(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed ({rc})")
+
+    def ceilings(self, reps=20):
+        """GB/s of each pattern over buffers far larger than the last-level
+        cache; the reduce pattern at the step's level shapes (P slices of the
+        level's INT4 bytes + scales, back to back, and one output slice), with
+        copies rotated to >= ROT_BYTES."""
+        T = self.torch
+        GiB = 1 << 30
+        a = T.empty(2 * GiB, dtype=T.uint8, device="cuda")
+        a.fill_(3)
+        b = T.empty(2 * GiB, dtype=T.uint8, device="cuda")
+        sink = T.zeros(16, dtype=T.uint8, device="cuda")
+        A, B_, L = a.data_ptr(), b.data_ptr(), self.L
+        res = {}
+        us = loop_us([lambda: self._ok(L.zqp_copy(A, B_, GiB, self._st()), "copy"),
+                      lambda: self._ok(L.zqp_copy(A + GiB, B_ + GiB, GiB, self._st()), "copy")], reps)
+        res["copy_GBps"] = round(2 * GiB / (us * 1e-6) / 1e9, 1)
+        us = loop_us([lambda: self._ok(L.zqp_read(A, 2 * GiB, sink.data_ptr(), 0x9E3779B9, self._st()), "read")], reps)
+        res["read_GBps"] = round(2 * GiB / (us * 1e-6) / 1e9, 1)
+        us = loop_us([lambda: self._ok(L.zqp_write(B_, 2 * GiB, 7, self._st()), "write")], reps)
+        res["write_GBps"] = round(2 * GiB / (us * 1e-6) / 1e9, 1)
+        us = loop_us([lambda: b[:GiB].copy_(a[:GiB])], reps)
+        res["torch_copy_GBps"] = round(2 * GiB / (us * 1e-6) / 1e9, 1)
+        n = 452_984_832
+        streams = {}
+        for P, m in ((8, n // 8), (2, n // 2), (4, n // 8), (48, n // 384), (8, n)):
+            sl = (nb4(m) + 4 * nsc(m, GBLOCK) + 15) // 16 * 16
+            fp = (P + 1) * sl
+            nsets = max(1, min(2 * GiB // (P * sl), -(-ROT_BYTES // fp)))
+            nsets = min(nsets, 2 * GiB // sl)
+            runs = [lambda k=k: self._ok(L.zqp_streams(A + k * P * sl, P, sl, B_ + k * sl, self._st()), "streams")
+                    for k in range(nsets)]
+            us = loop_us(runs, max(reps, 2 * nsets))
+            key = f"P={P} m={m}"
+            streams[key] = {"GBps": round(fp / (us * 1e-6) / 1e9, 1), "us": round(us, 2), "rotated_sets": nsets}
+        res["reduce_pattern"] = streams
+        del a, b
+        T.cuda.empty_cache()
+        return res
+
+
+def workload_tiny(reps):
+    """tiny-1024x1024: one 1024 x 1024 fp16 weight, INT8 B = 256 -> fp16; the
+    fp32 gradient of the same shape from P = 2 ranks, INT4 B = 128, one level
+    (rank 0's half), final dequantisation.  Latency-bound (<= 5 MB per call):
+    each figure is the time per launch of back-to-back launches."""
+    import torch
+
+    import paper_2501_04266_amd as zq
+    from paper_2501_04266_amd import workloads as wl
+    n = wl.N_TINY
+    w = torch.from_numpy(wl.weights(n, "f16", key=[1, wl.ROLE_WEIGHT, 0, 0])).to("cuda")
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    wsc = torch.empty(nsc(n, WBLOCK), device="cuda")
+    y = torch.empty(n, dtype=torch.float16, device="cuda")
+    g = [torch.from_numpy(wl.normal_f32(n, 1e-3, key=[1, wl.ROLE_OWN_GRAD if r == 0 else wl.ROLE_PEER_GRAD, 0, r]))
+         .to("cuda") for r in range(2)]
+    gp = torch.empty(nb4(n), dtype=torch.uint8, device="cuda")
+    gs = torch.empty(nsc(n, GBLOCK), device="cuda")
+    m = n // 2
+    mb, ms = nb4(m), nsc(m, GBLOCK)
+    pin = torch.empty(2 * mb, dtype=torch.uint8, device="cuda")
+    sin = torch.empty(2 * ms, device="cuda")
+    for r in range(2):      # rank r's chunk 0 arrives as slice r of rank 0's receive buffer
+        zq.qgz_quantize(g[r][:m], GBLOCK, packed=pin[r * mb:(r + 1) * mb], scales=sin[r * ms:(r + 1) * ms])
+    rp = torch.empty(mb, dtype=torch.uint8, device="cuda")
+    rs = torch.empty(ms, device="cuda")
+    gy = torch.empty(m, device="cuda")
+    runs = [
+        ("qwz_quantize", bytes_qwz_quant(n, 2, WBLOCK), n,
+         lambda: zq.qwz_quantize(w, WBLOCK, codes=codes, scales=wsc)),
+        ("qwz_dequantize", bytes_qwz_deq(n, 2, WBLOCK), n, lambda: zq.qwz_dequantize(codes, wsc, WBLOCK, y=y)),
+        ("qgz_quantize", bytes_qgz_quant(n, 4, GBLOCK), n,
+         lambda: zq.qgz_quantize(g[0], GBLOCK, packed=gp, scales=gs)),
+        ("qgz_reduce_level P=2", bytes_reduce(2, m, GBLOCK), 2 * m,
+         lambda: zq.qgz_reduce_level(pin, sin, 2, m, GBLOCK, packed_out=rp, scales_out=rs)),
+        ("qgz_dequantize", bytes_qgz_deq(m, 4, GBLOCK), m, lambda: zq.qgz_dequantize(rp, rs, m, GBLOCK, y=gy)),
+    ]
+    return [call_figures(name, nb, el, loop_us([fn], reps)) for name, nb, el, fn in runs]
+
+
+def workload_13b(reps):
+    """gpt-1.3b-layer: the GPT-1.3B-shaped layer (12 h^2, h = 2048,
+    50,331,648 parameters): bf16 weight shard 1/8 -> INT8 B = 256, the
+    gathered layer -> bf16; fp32 gradient -> INT4 B = 128, one P = 8 level
+    (m = n/8) and its all-shares mode (m = n), the shard -> fp32.  Every
+    call's inputs rotate over copies totalling >= 1.1 GB."""
+    import torch
+
+    import paper_2501_04266_amd as zq
+    from paper_2501_04266_amd import workloads as wl
+    np = __import__("numpy")
+    n = wl.N_13B
+    s, m = n // SHARD, n // 8
+    w = torch.from_numpy(wl.weights(n, "bf16", key=[2, wl.ROLE_WEIGHT, 0, 0]).view(np.int16)).to("cuda").view(
+        torch.bfloat16)
+    codes = torch.empty(n, dtype=torch.int8, device="cuda")
+    wsc = torch.empty(nsc(n, WBLOCK), device="cuda")
+    zq.qwz_quantize(w, WBLOCK, codes=codes, scales=wsc)          # the gathered layer (all 8 shards)
+    y = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    g = torch.from_numpy(wl.normal_f32(n, 1e-3, key=[2, wl.ROLE_OWN_GRAD, 0, 0])).to("cuda")
+    gp = torch.empty(nb4(n), dtype=torch.uint8, device="cuda")
+    gs = torch.empty(nsc(n, GBLOCK), device="cuda")
+    zq.qgz_quantize(g, GBLOCK, packed=gp, scales=gs)
+    mb, ms = nb4(m), nsc(m, GBLOCK)
+    pin = torch.empty(8 * mb, dtype=torch.uint8, device="cuda")
+    sin = torch.empty(8 * ms, device="cuda")
+    pin[:mb].copy_(gp[:mb])
+    sin[:ms].copy_(gs[:ms])
+    for p in range(1, 8):
+        xs = torch.from_numpy(wl.normal_f32(m, 1e-3, key=[2, wl.ROLE_PEER_GRAD, 0, p])).to("cuda")
+        zq.qgz_quantize(xs, GBLOCK, packed=pin[p * mb:(p + 1) * mb], scales=sin[p * ms:(p + 1) * ms])
+    apin = torch.from_numpy(wl.random_bytes(8 * nb4(n), key=[2, wl.ROLE_MISC, 9, 0])).to("cuda")
+    asin = torch.from_numpy(wl.uniform_f32(8 * nsc(n, GBLOCK), *wl.ALL_SHARES_SCALES, key=[2, wl.ROLE_MISC, 9, 1])).to(
+        "cuda")
+    U8, F32 = torch.uint8, torch.float32
+    E = lambda k, dt: torch.empty(k, dtype=dt, device="cuda")
+    specs = [
+        ("qwz_quantize", bytes_qwz_quant(s, 2, WBLOCK), s,
+         lambda i, o: zq.qwz_quantize(i[0], WBLOCK, codes=o[0], scales=o[1]), [w[:s]],
+         [codes[:s], wsc[:nsc(s, WBLOCK)]]),
+        ("qwz_dequantize", bytes_qwz_deq(n, 2, WBLOCK), n, lambda i, o: zq.qwz_dequantize(i[0], i[1], WBLOCK, y=o[0]),
+         [codes, wsc], [y]),
+        ("qgz_quantize", bytes_qgz_quant(n, 4, GBLOCK), n,
+         lambda i, o: zq.qgz_quantize(i[0], GBLOCK, packed=o[0], scales=o[1]), [g], [gp, gs]),
+        ("qgz_reduce_level P=8", bytes_reduce(8, m, GBLOCK), 8 * m,
+         lambda i, o: zq.qgz_reduce_level(i[0], i[1], 8, m, GBLOCK, packed_out=o[0], scales_out=o[1]), [pin, sin],
+         [E(mb, U8), E(ms, F32)]),
+        ("qgz_reduce_level P=8 all-shares (m = n)", bytes_reduce(8, n, GBLOCK), 8 * n,
+         lambda i, o: zq.qgz_reduce_level(i[0], i[1], 8, n, GBLOCK, packed_out=o[0], scales_out=o[1]), [apin, asin],
+         [E(nb4(n), U8), E(nsc(n, GBLOCK), F32)]),
+        ("qgz_dequantize", bytes_qgz_deq(m, 4, GBLOCK), m, lambda i, o: zq.qgz_dequantize(i[0], i[1], m, GBLOCK, y=o[0]),
+         [gp[:mb], gs[:ms]], [E(m, F32)]),
+    ]
+    return timed_calls(specs, reps)
+
+
+def workload_edge(reps):
+    """outlier-edge-123456789: 123,456,789 fp32 elements (not a multiple of
+    any block), 0.02 * Student-t(3) with 0.1% of them x100 and zero groups:
+    INT8 B = 256 and INT4 B = 64, each quantised and dequantised to bf16.
+    Inputs rotate over copies totalling >= 1.1 GB."""
+    import torch
+
+    import paper_2501_04266_amd as zq
+    from paper_2501_04266_amd import workloads as wl
+    n = wl.N_EDGE
+    x = torch.from_numpy(wl.outlier_tensor(n, key=[5, wl.ROLE_WEIGHT, 0, 0])).to("cuda")
+    c8, s8 = zq.qwz_quantize(x, 256)
+    p4, s4 = zq.qgz_quantize(x, 64)
+    BF = torch.bfloat16
+    specs = [
+        ("qwz_quantize INT8 B=256", bytes_qwz_quant(n, 4, 256), n,
+         lambda i, o: zq.qwz_quantize(i[0], 256, codes=o[0], scales=o[1]), [x], [c8, s8]),
+        ("qwz_dequantize INT8 -> bf16", bytes_qwz_deq(n, 2, 256), n,
+         lambda i, o: zq.qwz_dequantize(i[0], i[1], 256, y=o[0]), [c8, s8],
+         [torch.empty(n, dtype=BF, device="cuda")]),
+        ("qgz_quantize INT4 B=64", bytes_qgz_quant(n, 4, 64), n,
+         lambda i, o: zq.qgz_quantize(i[0], 64, packed=o[0], scales=o[1]), [x], [p4, s4]),
+        ("qgz_dequantize INT4 -> bf16", bytes_qgz_deq(n, 2, 64), n,
+         lambda i, o: zq.qgz_dequantize(i[0], i[1], n, 64, y=o[0]), [p4, s4],
+         [torch.empty(n, dtype=BF, device="cuda")]),
+    ]
+    return timed_calls(specs, reps)
+
+
+def step_call_specs(L):
+    """(name, bytes, elements, fn, inputs, outputs) of each call of the step,
+    on the step's own buffers."""
+    zq = L.zq
+    s = L.shard
+    specs = [
+        (lambda i, o: zq.qwz_quantize(i[0], WBLOCK, codes=o[0], scales=o[1]), [L.w[:s]],
+         [L.codes[:s], L.wscales[:nsc(s, WBLOCK)]]),
+        (lambda i, o: zq.qwz_dequantize(i[0], i[1], WBLOCK, y=o[0]), [L.codes, L.wscales], [L.y]),
+        (lambda i, o: zq.qgz_quantize(i[0], GBLOCK, packed=o[0], scales=o[1]), [L.g], [L.gp, L.gs]),
+        (lambda i, o: zq.qgz_reduce_level(i[0], i[1], 8, L.m8, GBLOCK, packed_out=o[0], scales_out=o[1]),
+         list(L.d8), list(L.o8)),
+        (lambda i, o: zq.qgz_dequantize(i[0], i[1], L.m8, GBLOCK, y=o[0]), list(L.o8), [L.gshard]),
+    ]
+    for P, m, d, o in L.chain:
+        specs.append((lambda i, o_, P=P, m=m: zq.qgz_reduce_level(i[0], i[1], P, m, GBLOCK, packed_out=o_[0],
+                                                                  scales_out=o_[1]), list(d), list(o)))
+    P, m, d, o = L.chain[-1]
+    specs.append((lambda i, o_, m=m: zq.qgz_dequantize(i[0], i[1], m, GBLOCK, y=o_[0]), list(o), [L.final]))
+    return [(name, b, e, fn, ins, outs) for (name, b, e), (fn, ins, outs) in zip(L.calls, specs)]
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--settle", type=int, default=100,
+                    help="steps run after the warm-up, before timing, while the GPU's clock settles")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
     ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
     ap.add_argument("--no-single-thread", action="store_true", help="skip the 1-thread oracle step")
     ap.add_argument("--steps-gemm", type=int, default=10, help="timed repetitions of the layer's GEMMs")
+    ap.add_argument("--no-extras", action="store_true", help="the step only (no other workloads, ceilings or GEMMs)")
     ap.add_argument("--n", type=int, default=0, help=argparse.SUPPRESS)  # smaller layer for quick checks
     args = ap.parse_args()
 
@@ -492,148 +802,64 @@ def main():
     dom = max(range(ncalls), key=lambda i: per_call_ms[i])
     dom_name, dom_bytes, _ = L.calls[dom]
 
+    # settle, right before the timed region: the clock falls for some tens of
+    # milliseconds once continuous heavy work starts (also after the breakdown
+    # pass, whose events leave short idle gaps), then recovers; blocks of 10
+    # steps are timed to report the transient
+    blocks = [min(10, args.settle - k) for k in range(0, args.settle, 10)]
+    sev = [torch.cuda.Event(enable_timing=True) for _ in range(len(blocks) + 1)]
+    sev[0].record()
+    for j, nb_ in enumerate(blocks):
+        for _ in range(nb_):
+            L.step()
+        sev[j + 1].record()
+    torch.cuda.synchronize()
+    settle = [sev[j].elapsed_time(sev[j + 1]) / nb_ for j, nb_ in enumerate(blocks)]
+    log(f"settle {args.settle} steps: " + " ".join(f"{v:.3f}" for v in settle))
+
     # timed region: K steps; the only events recorded are the pair around the
     # dominant kernel, which gives the roofline figure
     dev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    r0.record()
     for k in range(args.steps):
         L.step(dev[k], around=dom)
+    r1.record()
+    t_enq = time.perf_counter()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    gpu_ms_per_step = r0.elapsed_time(r1) / args.steps
+    enqueue_ms_per_step = (t_enq - t0) * 1e3 / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (GPU events {gpu_ms_per_step:.3f}, "
+        f"host enqueue {enqueue_ms_per_step:.3f})")
     dom_ms = np.array([dev[k][0].elapsed_time(dev[k][1]) for k in range(args.steps)])
 
     step_bytes = sum(b for _, b, _ in L.calls)
     step_elems = sum(e for _, _, e in L.calls)
     value = step_bytes / (ms_per_step * 1e-3) / 1e9
-    kernels = []
-    for (name, b, e), ms, med in zip(L.calls, per_call_ms, per_call_med):
-        k = {"call": name, "bytes": b, "elements": e, "us": round(ms * 1e3, 2), "us_median": round(med * 1e3, 2),
-             "GBps": round(b / (ms * 1e-3) / 1e9, 1), "Gelem_per_s": round(e / (ms * 1e-3) / 1e9, 1)}
-        valu = load_valu(name)
-        if valu is not None:
-            k["valu"] = valu
-        kernels.append(k)
     achieved = dom_bytes / (dom_ms.mean() * 1e-3) / 1e9
     traffic = load_traffic(dom_name)
 
-    # next row: the last level fused with the final dequantisation, against the
-    # two separate calls it replaces (same inputs, same outputs bit for bit)
-    fused = {}
-    for label, (P, m, d, o), yout in (("P=8 level + dequant", (8, L.m8, L.d8, L.o8), L.gshard),
-                                      ("P=48 level + dequant", L.chain[-1], L.final)):
-        def separate():
-            zq.qgz_reduce_level(d[0], d[1], P, m, GBLOCK, packed_out=o[0], scales_out=o[1])
-            zq.qgz_dequantize(o[0], o[1], m, GBLOCK, y=yout)
-
-        def fused_call():
-            zq.qgz_reduce_dequantize(d[0], d[1], P, m, GBLOCK, y=yout)
-
-        times = {}
-        for name, fn in (("separate", separate), ("fused", fused_call)):
-            for _ in range(3):
-                fn()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(args.steps):
-                fn()
-            e1.record()
-            torch.cuda.synchronize()
-            times[name] = e0.elapsed_time(e1) * 1e3 / args.steps
-        fused_bytes = P * (nb4(m) + 4 * nsc(m, GBLOCK)) + 4 * m
-        fused[label] = {"separate_us": round(times["separate"], 2), "fused_us": round(times["fused"], 2),
-                        "fused_bytes": fused_bytes,
-                        "fused_GBps": round(fused_bytes / (times["fused"] * 1e-6) / 1e9, 1)}
-
-    # all-shares mode of the P=8 level: 8 slices of the whole layer (m = n),
-    # random INT4 codes and scales, for a bandwidth figure over 2.17 GB
-    pin = torch.from_numpy(wl.random_bytes(8 * nb4(n), key=[3, wl.ROLE_MISC, 9, 0])).to("cuda")
-    sin = torch.from_numpy(wl.uniform_f32(8 * nsc(n, GBLOCK), *wl.ALL_SHARES_SCALES,
-                                          key=[3, wl.ROLE_MISC, 9, 1])).to("cuda")
-    aop = torch.empty(nb4(n), dtype=torch.uint8, device="cuda")
-    aos = torch.empty(nsc(n, GBLOCK), dtype=torch.float32, device="cuda")
-    allsh = lambda: zq.qgz_reduce_level(pin, sin, 8, n, GBLOCK, packed_out=aop, scales_out=aos)
-    for _ in range(3):
-        allsh()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        allsh()
-    e1.record()
-    torch.cuda.synchronize()
-    as_us = e0.elapsed_time(e1) * 1e3 / args.steps
-    as_bytes = bytes_reduce(8, n, GBLOCK)
-    all_shares = {"qgz_reduce_level P=8 m=n us": round(as_us, 2), "bytes": as_bytes,
-                  "GBps": round(as_bytes / (as_us * 1e-6) / 1e9, 1)}
-    del pin, sin, aop, aos
-
-    # next row: the P=8 level reading its slices in place from 8 separate
-    # buffers through device pointer tables (how a receiver would read peers'
-    # send buffers mapped over xGMI) against the contiguous receive buffer
-    mb8, ms8 = nb4(L.m8), nsc(L.m8, GBLOCK)
-    gp_sl = [L.d8[0][p * mb8:(p + 1) * mb8].clone() for p in range(8)]
-    gs_sl = [L.d8[1][p * ms8:(p + 1) * ms8].clone() for p in range(8)]
-    tables = zq.gather_tables(gp_sl, gs_sl)
-    go = (torch.empty(mb8, dtype=torch.uint8, device="cuda"), torch.empty(ms8, dtype=torch.float32, device="cuda"))
-    gather_call = lambda: zq.qgz_reduce_level_gather(gp_sl, gs_sl, L.m8, GBLOCK, packed_out=go[0], scales_out=go[1],
-                                                     tables=tables)
-    contig_call = lambda: zq.qgz_reduce_level(L.d8[0], L.d8[1], 8, L.m8, GBLOCK, packed_out=L.o8[0],
-                                              scales_out=L.o8[1])
-    gtimes = {}
-    for name, fn in (("contiguous", contig_call), ("gather", gather_call)):
-        for _ in range(3):
-            fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        gtimes[name] = e0.elapsed_time(e1) * 1e3 / args.steps
-    same = bool(torch.equal(go[0], L.o8[0]) and torch.equal(go[1], L.o8[1]))
-    gather = {"P=8 level contiguous us": round(gtimes["contiguous"], 2), "P=8 level gather us": round(gtimes["gather"], 2),
-              "gather_GBps": round(bytes_reduce(8, L.m8, GBLOCK) / (gtimes["gather"] * 1e-6) / 1e9, 1),
-              "bit_identical": same}
-    del gp_sl, gs_sl, tables, go
-
-    # next row: the degree-2 weight partition (1/2 shard quantised into its slot
-    # of the gathered buffer; the dequantisation of the gathered layer is the
-    # same call as in the step)
-    half = n // 2
-    sd2 = lambda: zq.qwz_quantize(L.w[:half], WBLOCK, codes=L.codes[:half], scales=L.wscales[:nsc(half, WBLOCK)])
-    for _ in range(3):
-        sd2()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(args.steps):
-        sd2()
-    e1.record()
-    torch.cuda.synchronize()
-    sd2_us = e0.elapsed_time(e1) * 1e3 / args.steps
-    sd2_bytes = bytes_qwz_quant(half, 2, WBLOCK)
-    sec_degree_2 = {"qwz_quantize half-shard us": round(sd2_us, 2), "bytes": sd2_bytes,
-                    "GBps": round(sd2_bytes / (sd2_us * 1e-6) / 1e9, 1)}
-
-    # next row: the layer's forward GEMMs with the gathered INT8 weight
-    # dequantised on load (qwz_dequant_gemm), 8192 tokens of bf16 activations,
-    # against dequantising the layer to bf16 and running torch's GEMM on it
-    dq_gemm = gemm_figures(L, args.steps_gemm, log)
-
-    # practical ceiling: a plain device-to-device copy of 1 GiB
-    src = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    for _ in range(3):
-        dst.copy_(src)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(COPY_REPS):
-        dst.copy_(src)
-    e1.record()
-    torch.cuda.synchronize()
-    copy_gbps = COPY_REPS * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    del src, dst
+    # per call: rotated back-to-back loops, the step's event brackets, the
+    # committed trace's kernel-only duration
+    kernels = timed_calls(step_call_specs(L), 40)
+    for k, ms, med in zip(kernels, per_call_ms, per_call_med):
+        k["us_in_step_events"] = round(ms * 1e3, 2)
+        k["us_in_step_events_median"] = round(med * 1e3, 2)
+        tr = load_trace(k["call"])
+        if tr is not None:
+            k["us_trace"] = tr
+            k["pct_hbm_peak_trace"] = round(100 * k["bytes"] / (tr * 1e-6) / 1e9 / HBM_PEAK_GBPS, 1)
+        valu = load_valu(k["call"])
+        if valu is not None:
+            k["valu"] = valu
+        if k["bytes"] >= GATE_BYTES:
+            k["gate_70pct"] = {"loop": k["pct_hbm_peak"] >= 70.0, "trace": (k.get("pct_hbm_peak_trace", 0) >= 70.0
+                                                                          if tr is not None else None)}
+    log("per-call loops done")
 
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
@@ -645,19 +871,20 @@ def main():
                                "P=8 level + 3-level chain P=2/4/48, final dequant -> fp32",
                    "n": n, "step_bytes": step_bytes, "step_elements": step_elems,
                    "pct_hbm_peak": round(100 * value / HBM_PEAK_GBPS, 1),
-                   "elements_per_s": round(step_elems / (ms_per_step * 1e-3))},
+                   "elements_per_s": round(step_elems / (ms_per_step * 1e-3)),
+                   "ms_per_step_gpu_events": round(gpu_ms_per_step, 4),
+                   "host_enqueue_ms_per_step": round(enqueue_ms_per_step, 4),
+                   "settle_steps": args.settle,
+                   "settle_ms_per_step_by_10": [round(v, 4) for v in settle]},
         "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "us_per_launch": round(dom_ms.mean() * 1e3, 2),
                      "us_median": round(float(np.median(dom_ms)) * 1e3, 2)},
         "kernels": kernels,
-        "fused_last_level": fused,
-        "sec_degree_2": sec_degree_2,
-        "all_shares": all_shares,
-        "reduce_gather": gather,
-        "dequant_gemm": dq_gemm,
-        "copy_ceiling_GBps": round(copy_gbps, 1),
     }
+
+    if not args.no_extras:
+        extras(L, args, out, log)
 
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or max(1, len(os.sched_getaffinity(0)))
@@ -677,6 +904,113 @@ def main():
         out["parity"] = "bit-exact vs oracle (all step outputs)" if not bad else f"MISMATCH: {bad}"
         log(f"oracle {secs:.1f}s; parity: {out['parity']}")
     print(json.dumps(out), flush=True)
+
+
+def extras(L, args, out, log):
+    """The fields measured after the timed region (see the module docstring)."""
+    import torch
+
+    from paper_2501_04266_amd import workloads as wl
+    zq, n = L.zq, L.n
+    reps = max(args.steps, 20)
+
+    # the other workloads, call by call
+    out["workloads"] = {"tiny-1024x1024 (latency-bound)": workload_tiny(max(reps, 100)),
+                        "gpt-1.3b-layer": workload_13b(reps),
+                        "outlier-edge-123456789": workload_edge(reps)}
+    log("workloads done")
+
+    # bandwidth ceilings of plain access patterns (hand-written kernels)
+    out["ceilings"] = Probe().ceilings()
+    out["copy_ceiling_GBps"] = out["ceilings"]["copy_GBps"]
+    log(f"ceilings: {out['ceilings']['copy_GBps']} GB/s copy")
+
+    # next row: the last level fused with the final dequantisation, against the
+    # two separate calls it replaces (same inputs, same outputs bit for bit)
+    fused = {}
+    for label, (P, m, d, o), yout in (("P=8 level + dequant", (8, L.m8, L.d8, L.o8), L.gshard),
+                                      ("P=48 level + dequant", L.chain[-1], L.final)):
+        sep_fn = lambda i, o_, P=P, m=m, yout=yout: (
+            zq.qgz_reduce_level(i[0], i[1], P, m, GBLOCK, packed_out=o_[0], scales_out=o_[1]),
+            zq.qgz_dequantize(o_[0], o_[1], m, GBLOCK, y=o_[2]))
+        fus_fn = lambda i, o_, P=P, m=m: zq.qgz_reduce_dequantize(i[0], i[1], P, m, GBLOCK, y=o_[2])
+        outs = [o[0], o[1], yout]
+        t_sep = loop_us(rotation_runs(sep_fn, list(d), outs), reps)
+        t_fus = loop_us(rotation_runs(fus_fn, list(d), outs), reps)
+        fused_bytes = P * (nb4(m) + 4 * nsc(m, GBLOCK)) + 4 * m
+        fused[label] = {"separate_us": round(t_sep, 2), "fused_us": round(t_fus, 2), "fused_bytes": fused_bytes,
+                        "fused_GBps": round(fused_bytes / (t_fus * 1e-6) / 1e9, 1)}
+        torch.cuda.empty_cache()
+    out["fused_last_level"] = fused
+
+    # all-shares mode of the P=8 level: 8 slices of the whole layer (m = n),
+    # random INT4 codes and scales, 2.17 GB per launch (beyond the cache):
+    # the first launches after the legs before it, then (the headline figure)
+    # the same after ALL_SHARES_SETTLE_S seconds of launches, once the clock
+    # has recovered from the dip that sustained reduce work causes
+    pin = torch.from_numpy(wl.random_bytes(8 * nb4(n), key=[3, wl.ROLE_MISC, 9, 0])).to("cuda")
+    sin = torch.from_numpy(wl.uniform_f32(8 * nsc(n, GBLOCK), *wl.ALL_SHARES_SCALES,
+                                          key=[3, wl.ROLE_MISC, 9, 1])).to("cuda")
+    aop = torch.empty(nb4(n), dtype=torch.uint8, device="cuda")
+    aos = torch.empty(nsc(n, GBLOCK), dtype=torch.float32, device="cuda")
+    allsh = lambda: zq.qgz_reduce_level(pin, sin, 8, n, GBLOCK, packed_out=aop, scales_out=aos)
+    first_us = loop_us([allsh], reps, warm=0)           # right after the lighter legs before it
+    t_end = time.perf_counter() + ALL_SHARES_SETTLE_S    # then the clock's dip and recovery
+    while time.perf_counter() < t_end:
+        for _ in range(8):
+            allsh()
+        torch.cuda.synchronize()
+    as_us = loop_us([allsh], reps, warm=0)
+    as_bytes = bytes_reduce(8, n, GBLOCK)
+    out["all_shares"] = {"qgz_reduce_level P=8 m=n us": round(as_us, 2), "bytes": as_bytes,
+                         "GBps": round(as_bytes / (as_us * 1e-6) / 1e9, 1),
+                         "pct_hbm_peak": round(100 * as_bytes / (as_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 1),
+                         "settle_s": ALL_SHARES_SETTLE_S,
+                         "first_launches_us": round(first_us, 2),
+                         "first_launches_GBps": round(as_bytes / (first_us * 1e-6) / 1e9, 1)}
+    del pin, sin, aop, aos
+    torch.cuda.empty_cache()
+
+    # next row: the P=8 level reading its slices in place from 8 separate
+    # buffers through device pointer tables (how a receiver would read peers'
+    # send buffers mapped over xGMI) against the contiguous receive buffer;
+    # both over rotated copies
+    mb8, ms8 = nb4(L.m8), nsc(L.m8, GBLOCK)
+    nsets = 4
+    gsets = []
+    for _ in range(nsets):
+        gp_sl = [L.d8[0][p * mb8:(p + 1) * mb8].clone() for p in range(8)]
+        gs_sl = [L.d8[1][p * ms8:(p + 1) * ms8].clone() for p in range(8)]
+        gsets.append((gp_sl, gs_sl, zq.gather_tables(gp_sl, gs_sl)))
+    csets = [(L.d8[0].clone(), L.d8[1].clone()) for _ in range(nsets)]
+    go = (torch.empty(mb8, dtype=torch.uint8, device="cuda"), torch.empty(ms8, dtype=torch.float32, device="cuda"))
+    co = (torch.empty(mb8, dtype=torch.uint8, device="cuda"), torch.empty(ms8, dtype=torch.float32, device="cuda"))
+    g_runs = [lambda s=s: zq.qgz_reduce_level_gather(s[0], s[1], L.m8, GBLOCK, packed_out=go[0], scales_out=go[1],
+                                                     tables=s[2]) for s in gsets]
+    c_runs = [lambda s=s: zq.qgz_reduce_level(s[0], s[1], 8, L.m8, GBLOCK, packed_out=co[0], scales_out=co[1])
+              for s in csets]
+    t_c, t_g = loop_us(c_runs, reps), loop_us(g_runs, reps)
+    same = bool(torch.equal(go[0], co[0]) and torch.equal(go[1], co[1]))
+    out["reduce_gather"] = {"P=8 level contiguous us": round(t_c, 2), "P=8 level gather us": round(t_g, 2),
+                            "gather_GBps": round(bytes_reduce(8, L.m8, GBLOCK) / (t_g * 1e-6) / 1e9, 1),
+                            "bit_identical": same, "rotated_sets": nsets}
+    del gsets, csets
+    torch.cuda.empty_cache()
+
+    # next row: the degree-2 weight partition (1/2 shard quantised into its slot
+    # of the gathered buffer; the dequantisation of the gathered layer is the
+    # same call as in the step)
+    half = n // 2
+    sd2_us = loop_us([lambda: zq.qwz_quantize(L.w[:half], WBLOCK, codes=L.codes[:half],
+                                              scales=L.wscales[:nsc(half, WBLOCK)])], reps)
+    sd2_bytes = bytes_qwz_quant(half, 2, WBLOCK)
+    out["sec_degree_2"] = {"qwz_quantize half-shard us": round(sd2_us, 2), "bytes": sd2_bytes,
+                           "GBps": round(sd2_bytes / (sd2_us * 1e-6) / 1e9, 1)}
+
+    # next row: the layer's forward GEMMs with the gathered INT8 weight
+    # dequantised on load (qwz_dequant_gemm), 8192 tokens of bf16 activations,
+    # against dequantising the layer to bf16 and running torch's GEMM on it
+    out["dequant_gemm"] = gemm_figures(L, args.steps_gemm, log)
 
 
 if __name__ == "__main__":

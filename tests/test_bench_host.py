@@ -71,3 +71,38 @@ def test_source_hash_covers_the_codec_sources():
     assert names == {"zq_kernels.hip", "zq_internal.h", "zq_device.h", "zq_host.h", "zq_api.hip"}
     assert all(os.path.exists(p) for p in bench.KERNEL_SOURCES)
     assert len(bench.kernel_source_hash()) == 16
+
+
+def test_rotation_covers_the_cache_and_binds_separate_buffers():
+    import torch
+    x = torch.zeros(1000, dtype=torch.uint8)
+    y = torch.zeros(1000, dtype=torch.uint8)
+    seen = []
+    runs = bench.rotation_runs(lambda i, o: seen.append((i[0].data_ptr(), o[0].data_ptr())), [x], [y],
+                               footprint=bench.ROT_BYTES // 3 + 1)
+    assert len(runs) == 3
+    for r in runs:
+        r()
+    assert seen[0] == (x.data_ptr(), y.data_ptr())
+    assert len({a for a, _ in seen}) == 3 and len({b for _, b in seen}) == 3
+    assert len(bench.rotation_runs(lambda i, o: None, [x], [y], footprint=2 * bench.ROT_BYTES)) == 1
+
+
+def test_trace_summary_is_used_only_for_the_sources_it_was_taken_on(tmp_path, monkeypatch):
+    trace = _profile(tmp_path, "trace.txt",
+                     "# kernel source sha256[:16]: 0123456789abcdef\n"
+                     "call  kernel  grid  trace avg us  min  max  event us\n"
+                     "qgz_reduce_level P=8  k_reduce_p<128, 32, 8, 1, -1, false>  1769472  45.10  44.00  47.00  50.20\n"
+                     "qgz_reduce_level P=48  k_reduce<128, 8, 16, 1, false, -1, false>  147456  12.24  11.60  14.40  17.10\n")
+    monkeypatch.setattr(bench, "TRACE_PROFILE", trace)
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "0123456789abcdef")
+    assert bench.load_trace("qgz_reduce_level P=8") == 45.10
+    assert bench.load_trace("qgz_reduce_level P=48") == 12.24
+    assert bench.load_trace("qgz_reduce_level P=4") is None
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: "fedcba9876543210")
+    assert bench.load_trace("qgz_reduce_level P=8") is None
+
+
+def test_call_figures():
+    f = bench.call_figures("x", 8_000_000_000, 1_000_000_000, 1_000.0)
+    assert f["GBps"] == 8000.0 and f["pct_hbm_peak"] == 100.0 and f["Gelem_per_s"] == 1000.0
