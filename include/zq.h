@@ -39,7 +39,8 @@
  * Conventions for every call:
  *   - All array pointers are device pointers (hipMalloc'd or equivalent) in
  *     the caller's ownership; the library allocates nothing and keeps no
- *     state between calls.
+ *     state between calls, except the device address table of
+ *     qgz_reduce_level_gather_noalloc (a static array per GPU).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL = the default stream)
  *     and returns without synchronising; results are visible after the
  *     stream is synchronised.  Calls from several host threads are safe.

@@ -2,7 +2,8 @@
 // the host, grid sizing, and launches on the caller's stream.
 //
 // Every check runs before anything is enqueued, so an argument error writes
-// no output byte.  The library allocates nothing and keeps no state.  Each
+// no output byte.  The library allocates nothing; its only state is the
+// static address table of the allocation-free gathered reduce.  Each
 // launch covers its whole tensor (one tile per wave), so the grid size follows
 // from n alone.
 #include <hip/hip_runtime.h>
@@ -37,22 +38,17 @@ int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, floa
   if (any_overlap({{out, out_bytes}, {scales, 4 * nb}}, {{x, n * elem_bytes(xt)}})) return ZQ_E_ALIAS;
 
   const int64_t nfull = n / block;
-  const int64_t blocks_per_wave = 64 / (block / quant_elems((int)elem_bytes(xt), block));
-  const int64_t grid = grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64 * kQuantTiles);
-  if (grid == 0) return ZQ_E_SIZE;
-
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  int rc = ZQ_OK;
-  if (nfull > 0) {
-    rc = launch(quant_kernel(xt, qbits, lgB), (unsigned)grid, kQuantThreads, st, x, nfull, out, scales);
-    if (rc != ZQ_OK) return rc;
-  }
   const int64_t rest = n - nfull * block;
-  if (rest > 0) {
-    rc = launch(quant_tail_kernel(xt, qbits), 1u, 64u, st, x, nfull * (int64_t)block, (int)rest, out,
-                scales + nfull);
-  }
-  return rc;
+  const int64_t blocks_per_wave = 64 / (block / quant_elems((int)elem_bytes(xt), block));
+  // workgroups of full blocks, plus one for a short last block
+  const int64_t full_wgs =
+      nfull > 0 ? grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64 * kQuantTiles) : 0;
+  if (nfull > 0 && full_wgs == 0) return ZQ_E_SIZE;
+  const int64_t grid = full_wgs + (rest > 0 ? 1 : 0);
+  if (grid > kMaxGrid) return ZQ_E_SIZE;
+
+  return launch(quant_kernel(xt, qbits, lgB), (unsigned)grid, kQuantThreads, static_cast<hipStream_t>(stream), x,
+                nfull, out, scales, (int)rest);
 }
 
 int dequantize(const void* codes, const float* scales, int64_t n, int32_t block, void* y, int yt, void* stream,

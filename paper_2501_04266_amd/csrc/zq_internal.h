@@ -78,15 +78,14 @@ constexpr int reduce_tiles(ReduceShape s) {
 #define ZQ_REDUCE_SMALL_WAVES 4096
 #endif
 
-using QuantKernel = void (*)(const void*, int64_t, uint8_t*, float*);
-using QuantTailKernel = void (*)(const void*, int64_t, int, uint8_t*, float*);
+// (x, full blocks, out, scales, length of the short last block or 0)
+using QuantKernel = void (*)(const void*, int64_t, uint8_t*, float*, int);
 using DequantKernel = void (*)(const uint8_t*, const float*, int64_t, int, void*);
 using ReduceKernel = void (*)(const uint8_t*, const float*, int, int64_t, int64_t, int64_t, uint8_t*, float*, void*);
 using ReduceGenericKernel = void (*)(const uint8_t*, const float*, int, int64_t, int64_t, int64_t, int, int64_t,
                                      uint8_t*, float*, void*, int);
 
 QuantKernel quant_kernel(int dt, int qbits, int lgB);
-QuantTailKernel quant_tail_kernel(int dt, int qbits);
 DequantKernel dequant_kernel(int dt, int qbits);
 // ydt < 0: INT4 output only; otherwise also the fused dequantisation to ydt
 ReduceKernel reduce_kernel(int lgB, ReduceShape shape, int ydt);

@@ -270,11 +270,40 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
 // one contiguous run of 16-byte stores: at this kernel's ~8:1 read:write mix
 // that keeps the write stream from slowing the reads (per-lane 2-byte stores
 // measured ~10% slower).  A workgroup holding the last, partial tile stores
-// straight from its lanes instead.
+// straight from its lanes instead.  When n is not a multiple of B, one more
+// workgroup quantises the short last block, in the same launch.
+
+// The one short block [start, start + len), len < B <= 1024, quantised by
+// one wave; the scale goes to *scale.
+template <int DT, int QBITS>
+__device__ __forceinline__ void quantize_tail(const void* __restrict__ x, int64_t start, int len,
+                                              uint8_t* __restrict__ out, float* __restrict__ scale) {
+  constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
+  const int lane = threadIdx.x & 63;
+  float a = 0.0f;
+  for (int j = lane; j < len; j += 64) a = fmaxf(a, fabsf(load1<DT>(x, start + j)));
+  const float amax = u2f(wave_max(f2u(a)));
+  float s = 0.0f, r = 0.0f;
+  if (amax >= kFlushBelow) {
+    s = scale_of<(int)QMAX>(amax);
+    r = QMAX / amax;
+  }
+  if constexpr (QBITS == 8) {
+    for (int j = lane; j < len; j += 64) out[start + j] = (uint8_t)code_bits(load1<DT>(x, start + j), r);
+  } else {
+    for (int k = lane; 2 * k < len; k += 64) {
+      uint32_t lo = code_bits(load1<DT>(x, start + 2 * k), r);
+      uint32_t hi = (2 * k + 1 < len) ? code_bits(load1<DT>(x, start + 2 * k + 1), r) : 0u;
+      out[(start >> 1) + k] = (uint8_t)((lo & 0xfu) | ((hi & 0xfu) << 4));
+    }
+  }
+  if (lane == 0) *scale = s;
+}
 
 template <int DT, int QBITS, int B>
 __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restrict__ x, int64_t nfull,
-                                                            uint8_t* __restrict__ out, float* __restrict__ scales) {
+                                                            uint8_t* __restrict__ out, float* __restrict__ scales,
+                                                            int tail) {
   constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
   constexpr int T = kQuantTiles, WAVES = kQuantThreads / 64;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
@@ -287,6 +316,12 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   __shared__ float sbuf[WG_BLOCKS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // the workgroup after those of the full blocks quantises the short last
+  // block (tail elements) with its first wave
+  if ((int64_t)blockIdx.x * WG_BLOCKS >= nfull) {
+    if (wave == 0 && tail > 0) quantize_tail<DT, QBITS>(x, nfull * B, tail, out, scales + nfull);
+    return;
+  }
   // workgroup g owns tiles [g*WAVES*T, (g+1)*WAVES*T); its t-th round of loads
   // covers WAVES adjacent tiles, one per wave
   const int64_t wg_blk0 = (int64_t)blockIdx.x * WG_BLOCKS;
@@ -357,32 +392,6 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
     for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<ZQ_NT_QUANT>(dst + c, obuf[c]);
     if (tid < WG_BLOCKS) st<2 * ZQ_NT_SCALES>(scales + wg_blk0 + tid, sbuf[tid]);
   }
-}
-
-// The one short block [start, start + len), len < B <= 1024; one wave.
-template <int DT, int QBITS>
-__global__ void __launch_bounds__(64) k_quantize_tail(const void* __restrict__ x, int64_t start, int len,
-                                                      uint8_t* __restrict__ out, float* __restrict__ scale) {
-  constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
-  const int lane = threadIdx.x;
-  float a = 0.0f;
-  for (int j = lane; j < len; j += 64) a = fmaxf(a, fabsf(load1<DT>(x, start + j)));
-  const float amax = u2f(wave_max(f2u(a)));
-  float s = 0.0f, r = 0.0f;
-  if (amax >= kFlushBelow) {
-    s = scale_of<(int)QMAX>(amax);
-    r = QMAX / amax;
-  }
-  if constexpr (QBITS == 8) {
-    for (int j = lane; j < len; j += 64) out[start + j] = (uint8_t)code_bits(load1<DT>(x, start + j), r);
-  } else {
-    for (int k = lane; 2 * k < len; k += 64) {
-      uint32_t lo = code_bits(load1<DT>(x, start + 2 * k), r);
-      uint32_t hi = (2 * k + 1 < len) ? code_bits(load1<DT>(x, start + 2 * k + 1), r) : 0u;
-      out[(start >> 1) + k] = (uint8_t)((lo & 0xfu) | ((hi & 0xfu) << 4));
-    }
-  }
-  if (lane == 0) *scale = s;
 }
 
 // ------------------------------------------------------------------ dequantise
@@ -839,17 +848,6 @@ QuantKernel quant_kernel(int dt, int qbits, int lgB) {
   if (dt == ZQ_F32) return quant_kernel_for<ZQ_F32, 4>(lgB);
   if (dt == ZQ_F16) return quant_kernel_for<ZQ_F16, 4>(lgB);
   return quant_kernel_for<ZQ_BF16, 4>(lgB);
-}
-
-QuantTailKernel quant_tail_kernel(int dt, int qbits) {
-  if (qbits == 8) {
-    if (dt == ZQ_F32) return &k_quantize_tail<ZQ_F32, 8>;
-    if (dt == ZQ_F16) return &k_quantize_tail<ZQ_F16, 8>;
-    return &k_quantize_tail<ZQ_BF16, 8>;
-  }
-  if (dt == ZQ_F32) return &k_quantize_tail<ZQ_F32, 4>;
-  if (dt == ZQ_F16) return &k_quantize_tail<ZQ_F16, 4>;
-  return &k_quantize_tail<ZQ_BF16, 4>;
 }
 
 DequantKernel dequant_kernel(int dt, int qbits) {

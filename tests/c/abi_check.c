@@ -172,6 +172,15 @@ int main(void) {
       HIP_OK(hipStreamSynchronize(st));
       compare(grp, orp, mb, "gather packed");
       compare(grs, ors, ms * sizeof(float), "gather scales");
+      /* the allocation-free form: the same addresses from host arrays */
+      HIP_OK(hipMemset(grp, 0xA5, mb));
+      HIP_OK(hipMemset(grs, 0xA5, ms * sizeof(float)));
+      expect_status(qgz_reduce_level_gather_noalloc(hp, hs, P, m, B, grp, grs, st), ZQ_OK,
+                    "qgz_reduce_level_gather_noalloc");
+      HIP_OK(hipStreamSynchronize(st));
+      compare(grp, orp, mb, "gather (no alloc) packed");
+      compare(grs, ors, ms * sizeof(float), "gather (no alloc) scales");
+      expect_status(qgz_reduce_level_gather_noalloc(hp, hs, 1025, m, B, grp, grs, st), ZQ_E_P, "no-alloc P = 1025");
       HIP_OK(hipFree((void*)tp)); HIP_OK(hipFree((void*)ts)); HIP_OK(hipFree(grp)); HIP_OK(hipFree(grs));
     }
     HIP_OK(hipFree(dg)); HIP_OK(hipFree(dq)); HIP_OK(hipFree(dqs)); HIP_OK(hipFree(dpin)); HIP_OK(hipFree(dsin));
