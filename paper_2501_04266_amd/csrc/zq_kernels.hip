@@ -316,10 +316,11 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   __shared__ float sbuf[WG_BLOCKS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // the workgroup after those of the full blocks quantises the short last
-  // block (tail elements) with its first wave
-  if ((int64_t)blockIdx.x * WG_BLOCKS >= nfull) {
-    if (wave == 0 && tail > 0) quantize_tail<DT, QBITS>(x, nfull * B, tail, out, scales + nfull);
+  // with a short last block (tail > 0 elements) the launch has one workgroup
+  // more than the full blocks need: the last one quantises that block with
+  // its first wave (scalar test: 32-bit workgroup indices)
+  if (tail > 0 && blockIdx.x == gridDim.x - 1) {
+    if (wave == 0) quantize_tail<DT, QBITS>(x, nfull * B, tail, out, scales + nfull);
     return;
   }
   // workgroup g owns tiles [g*WAVES*T, (g+1)*WAVES*T); its t-th round of loads
