@@ -475,3 +475,47 @@ def test_reduce_edge_sums(kind, P, block, m):
     torch.cuda.synchronize()
     assert_bits_equal(from_dev(hp), po, f"{what} gather packed", block // 2)
     assert_bits_equal(from_dev(hs), so, f"{what} gather scales")
+
+
+# The compile-time-P kernel (P = 2, 4, 8; B = 64, 128, 256) at sizes where its
+# workgroups take T = 4 groups (P = 2) and the group count leaves 1, 2 or 3
+# over, so the last workgroup clamps to the last group and recomputes it;
+# some sizes also leave a block for the generic kernel.  Plain, fused (f32,
+# bf16) and gathered.
+FIXED_P_CASES = [(2, 128, 8192 * 4097), (2, 128, 8192 * 4098 + 128), (2, 256, 8192 * 4099),
+                 (2, 64, 8192 * 4097 + 64), (4, 64, 8192 * 4098), (4, 256, 8192 * 4099),
+                 (8, 64, 8192 * 4098), (8, 256, 8192 * 4097)]
+
+
+def _random_level(P, m, block, seed):
+    """P slices of random bytes (every nibble value, -8 included; m is even)
+    and scales in [1e-4, 1e-3)."""
+    assert m % 2 == 0
+    g = np.random.default_rng(seed)
+    packed = g.integers(0, 256, P * (m // 2), dtype=np.uint8)
+    scales = g.uniform(1e-4, 1e-3, P * ((m + block - 1) // block)).astype(np.float32)
+    return packed, scales
+
+
+@pytest.mark.parametrize("P,block,m", FIXED_P_CASES)
+def test_reduce_fixed_p_group_tails(P, block, m):
+    what = f"P={P} B={block} m={m}"
+    pin, sin = _random_level(P, m, block, 13 * P + block + m)
+    po, so = oracle.qgz_reduce_level(pin, sin, P, m, block)
+    dpin, dsin = to_dev(pin), to_dev(sin)
+    nb, mb = zq.num_scales(m, block), zq.int4_bytes(m)
+    gp, gs = poisoned(mb, torch.uint8), poisoned(nb, torch.float32)
+    zq.qgz_reduce_level(dpin, dsin, P, m, block, packed_out=gp, scales_out=gs)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(gp), po, f"{what} packed", block // 2)
+    assert_bits_equal(from_dev(gs), so, f"{what} scales")
+    for out, dt in (("f32", torch.float32), ("bf16", torch.bfloat16)):
+        y = zq.qgz_reduce_dequantize(dpin, dsin, P, m, block, out_dtype=dt)
+        torch.cuda.synchronize()
+        assert_bits_equal(from_dev(y), oracle.qgz_dequantize(po, so, m, block, out), f"{what} fused -> {out}")
+    ps = [dpin[p * mb:(p + 1) * mb].clone() for p in range(P)]
+    ss = [dsin[p * nb:(p + 1) * nb].clone() for p in range(P)]
+    hp, hs = zq.qgz_reduce_level_gather(ps, ss, m, block)
+    torch.cuda.synchronize()
+    assert_bits_equal(from_dev(hp), po, f"{what} gather packed", block // 2)
+    assert_bits_equal(from_dev(hs), so, f"{what} gather scales")
