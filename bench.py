@@ -600,7 +600,8 @@ def workload_tiny(reps):
     """tiny-1024x1024: one 1024 x 1024 fp16 weight, INT8 B = 256 -> fp16; the
     fp32 gradient of the same shape from P = 2 ranks, INT4 B = 128, one level
     (rank 0's half), final dequantisation.  Latency-bound (<= 5 MB per call):
-    each figure is the time per launch of back-to-back launches."""
+    each figure is the time per launch of back-to-back launches; then the
+    whole path eagerly and as one HIP graph replay."""
     import torch
 
     import paper_2501_04266_amd as zq
@@ -633,7 +634,36 @@ def workload_tiny(reps):
          lambda: zq.qgz_reduce_level(pin, sin, 2, m, GBLOCK, packed_out=rp, scales_out=rs)),
         ("qgz_dequantize", bytes_qgz_deq(m, 4, GBLOCK), m, lambda: zq.qgz_dequantize(rp, rs, m, GBLOCK, y=gy)),
     ]
-    return [call_figures(name, nb, el, loop_us([fn], reps)) for name, nb, el, fn in runs]
+    figs = [call_figures(name, nb, el, loop_us([fn], reps)) for name, nb, el, fn in runs]
+
+    # the whole path (five calls) launched eagerly against replayed from one
+    # HIP graph (the calls enqueue only kernels, so they can be captured);
+    # every output of a replay must equal the eager outputs bit for bit
+    def path():
+        for _, _, _, fn in runs:
+            fn()
+
+    path()
+    torch.cuda.synchronize()
+    outs = (codes, wsc, y, gp, gs, rp, rs, gy)
+    want = [t.clone() for t in outs]
+    eager_us = loop_us([path], reps)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(graph, stream=s):
+            path()
+    torch.cuda.synchronize()
+    for t in outs:
+        t.zero_()
+    graph.replay()
+    torch.cuda.synchronize()
+    same = all(torch.equal(a.view(torch.uint8), b.view(torch.uint8)) for a, b in zip(outs, want))
+    graph_us = loop_us([graph.replay], reps)
+    figs.append({"call": "whole path (5 calls)", "eager_us": round(eager_us, 2), "graph_replay_us": round(graph_us, 2),
+                 "graph_bit_identical": same})
+    return figs
 
 
 def workload_13b(reps):
