@@ -42,7 +42,9 @@ int quantize(const void* x, int xt, int64_t n, int32_t block, uint8_t* out, floa
   const int64_t blocks_per_wave = 64 / (block / quant_elems((int)elem_bytes(xt), block));
   // workgroups of full blocks, plus one for a short last block
   const int64_t full_wgs =
-      nfull > 0 ? grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave, kQuantThreads / 64 * kQuantTiles) : 0;
+      nfull > 0 ? grid_for((nfull + blocks_per_wave - 1) / blocks_per_wave,
+                           kQuantThreads / 64 * quant_tiles((int)elem_bytes(xt)))
+                : 0;
   if (nfull > 0 && full_wgs == 0) return ZQ_E_SIZE;
   const int64_t grid = full_wgs + (rest > 0 ? 1 : 0);
   if (grid > kMaxGrid) return ZQ_E_SIZE;

@@ -10,10 +10,16 @@ constexpr int kThreads = 256;  // threads per workgroup of the streaming kernels
 #define ZQ_QUANT_THREADS 256
 #endif
 constexpr int kQuantThreads = ZQ_QUANT_THREADS;
-#ifndef ZQ_QUANT_TILES
-#define ZQ_QUANT_TILES 1
+// wave tiles per wave in the quantiser: one for fp32 input, two for 16-bit
+// input (fewer, longer waves suit its smaller loads; on fp32 they measured
+// slower)
+#ifndef ZQ_QUANT_TILES_F32
+#define ZQ_QUANT_TILES_F32 1
 #endif
-constexpr int kQuantTiles = ZQ_QUANT_TILES;  // wave tiles per wave in the quantiser
+#ifndef ZQ_QUANT_TILES_16
+#define ZQ_QUANT_TILES_16 2
+#endif
+constexpr int quant_tiles(int dt_bytes) { return dt_bytes == 4 ? ZQ_QUANT_TILES_F32 : ZQ_QUANT_TILES_16; }
 #ifndef ZQ_DEQ_THREADS
 #define ZQ_DEQ_THREADS 256
 #endif

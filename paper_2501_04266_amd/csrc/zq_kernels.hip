@@ -305,7 +305,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
                                                             uint8_t* __restrict__ out, float* __restrict__ scales,
                                                             int tail) {
   constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
-  constexpr int T = kQuantTiles, WAVES = kQuantThreads / 64;
+  constexpr int T = quant_tiles(elem_size<DT>()), WAVES = kQuantThreads / 64;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
   constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane and tile
   constexpr int WG_BLOCKS = WAVES * T * BPW;                    // blocks per workgroup
