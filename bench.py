@@ -28,6 +28,9 @@ over its first ~40 steps; the breakdown pass's events leave idle gaps that
 let the clock rise again); then the timed region of K steps, host wall clock
 between two device synchronisations, with one event pair around the
 dominant kernel only (its per-launch duration gives the roofline figure).
+All events are HIP events without the system-scope fence (TimingEvent):
+torch's default events write back and invalidate the caches when recorded
+and cost about 3 us of GPU time each, fence-free ones about 1.7 us.
 The settle steps' times are reported too.
 
 Per-call figures (`kernels`): each call of the step launched back to back in
@@ -388,7 +391,7 @@ def gemm_figures(L, reps, log):
     def timed(fn):
         for _ in range(2):
             fn()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0, e1 = TimingEvent(), TimingEvent()
         e0.record()
         for _ in range(reps):
             fn()
@@ -459,6 +462,70 @@ def _tensor_bytes(ts):
     return sum(t.numel() * t.element_size() for t in ts)
 
 
+HIP_EVENT_DISABLE_SYSTEM_FENCE = 0x20000000  # hipEventDisableSystemFence
+
+
+class TimingEvent:
+    """A HIP event used only to take GPU timestamps, recorded on torch's
+    current stream (where the bindings launch).
+
+    It is created with hipEventDisableSystemFence: recording it does not
+    write back and invalidate the caches at system scope, which a default
+    event (torch.cuda.Event) does and which leaves a gap of several
+    microseconds between the launches around it.  Read it (elapsed_time)
+    only after a device synchronisation."""
+
+    _hip = None
+
+    @classmethod
+    def _runtime(cls):
+        if cls._hip is None:
+            import ctypes
+
+            import torch  # noqa: F401  (loads the HIP runtime that torch's streams belong to)
+            path = next((ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64.so" in ln),
+                        "libamdhip64.so")
+            hip = ctypes.CDLL(path)
+            vp = ctypes.c_void_p
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(vp), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [vp, vp]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), vp, vp]
+            hip.hipEventDestroy.argtypes = [vp]
+            for f in (hip.hipEventCreateWithFlags, hip.hipEventRecord, hip.hipEventElapsedTime,
+                      hip.hipEventDestroy):
+                f.restype = ctypes.c_int
+            cls._hip = hip
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+        self._hip = self._runtime()
+        self.h = ctypes.c_void_p()
+        self._check(self._hip.hipEventCreateWithFlags(ctypes.byref(self.h), HIP_EVENT_DISABLE_SYSTEM_FENCE),
+                    "hipEventCreateWithFlags")
+
+    @staticmethod
+    def _check(rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with HIP error {rc}")
+
+    def record(self):
+        import torch
+        self._check(self._hip.hipEventRecord(self.h, torch.cuda.current_stream().cuda_stream), "hipEventRecord")
+
+    def elapsed_time(self, end):
+        """Milliseconds from this event to `end`."""
+        import ctypes
+        ms = ctypes.c_float()
+        self._check(self._hip.hipEventElapsedTime(ctypes.byref(ms), self.h, end.h), "hipEventElapsedTime")
+        return ms.value
+
+    def __del__(self):
+        h = getattr(self, "h", None)
+        if h is not None and h.value:
+            self._hip.hipEventDestroy(h)
+
+
 def rotation_runs(fn, inputs, outputs, footprint=None):
     """Closures running fn(inputs, outputs) over enough copies of the inputs
     (and separate outputs) that one pass over them moves >= ROT_BYTES: a loop
@@ -481,7 +548,7 @@ def loop_us(runs, reps, warm=3):
     import torch
     for i in range(warm):
         runs[i % len(runs)]()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0, e1 = TimingEvent(), TimingEvent()
     e0.record()
     for i in range(reps):
         runs[i % len(runs)]()
@@ -820,9 +887,10 @@ def main():
     log(f"warmup {args.warmup} done")
 
     # breakdown pass (not the timed region): HIP events between all calls of
-    # each step; an event between two launches costs about 3 us of GPU time,
-    # so these figures are per call but the step time is not taken here
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(ncalls + 1)] for _ in range(args.steps)]
+    # each step; even a fence-free event between two launches costs about
+    # 1.7 us of GPU time, so these figures are per call but the step time is
+    # not taken here
+    evs = [[TimingEvent() for _ in range(ncalls + 1)] for _ in range(args.steps)]
     for k in range(args.steps):
         L.step(evs[k])
     torch.cuda.synchronize()
@@ -837,7 +905,7 @@ def main():
     # pass, whose events leave short idle gaps), then recovers; blocks of 10
     # steps are timed to report the transient
     blocks = [min(10, args.settle - k) for k in range(0, args.settle, 10)]
-    sev = [torch.cuda.Event(enable_timing=True) for _ in range(len(blocks) + 1)]
+    sev = [TimingEvent() for _ in range(len(blocks) + 1)]
     sev[0].record()
     for j, nb_ in enumerate(blocks):
         for _ in range(nb_):
@@ -849,8 +917,8 @@ def main():
 
     # timed region: K steps; the only events recorded are the pair around the
     # dominant kernel, which gives the roofline figure
-    dev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
-    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    dev = [[TimingEvent() for _ in range(2)] for _ in range(args.steps)]
+    r0, r1 = TimingEvent(), TimingEvent()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     r0.record()

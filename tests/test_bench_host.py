@@ -106,3 +106,14 @@ def test_trace_summary_is_used_only_for_the_sources_it_was_taken_on(tmp_path, mo
 def test_call_figures():
     f = bench.call_figures("x", 8_000_000_000, 1_000_000_000, 1_000.0)
     assert f["GBps"] == 8000.0 and f["pct_hbm_peak"] == 100.0 and f["Gelem_per_s"] == 1000.0
+
+
+def test_timing_event_binds_the_hip_runtime_torch_loaded():
+    # resolves the four event calls in the HIP runtime of this process (no
+    # GPU call is made: creating an event needs a device)
+    hip = bench.TimingEvent._runtime()
+    for name in ("hipEventCreateWithFlags", "hipEventRecord", "hipEventElapsedTime", "hipEventDestroy"):
+        assert getattr(hip, name).restype is not None
+    maps = [ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64.so" in ln]
+    assert maps and hip._name == maps[0]
+    assert bench.HIP_EVENT_DISABLE_SYSTEM_FENCE == 0x20000000
