@@ -10,14 +10,14 @@ constexpr int kThreads = 256;  // threads per workgroup of the streaming kernels
 #define ZQ_QUANT_THREADS 256
 #endif
 constexpr int kQuantThreads = ZQ_QUANT_THREADS;
-// wave tiles per wave in the quantiser: one for fp32 input, two for 16-bit
-// input (fewer, longer waves suit its smaller loads; on fp32 they measured
-// slower)
+// wave tiles per wave in the quantiser: one for either input width (two
+// tiles on 16-bit input measured slower than one tile of 16 elements per
+// lane; on fp32 input two tiles measured slower too)
 #ifndef ZQ_QUANT_TILES_F32
 #define ZQ_QUANT_TILES_F32 1
 #endif
 #ifndef ZQ_QUANT_TILES_16
-#define ZQ_QUANT_TILES_16 2
+#define ZQ_QUANT_TILES_16 1
 #endif
 constexpr int quant_tiles(int dt_bytes) { return dt_bytes == 4 ? ZQ_QUANT_TILES_F32 : ZQ_QUANT_TILES_16; }
 #ifndef ZQ_DEQ_THREADS
@@ -28,14 +28,18 @@ constexpr int kDeqThreads = ZQ_DEQ_THREADS;
 
 // Elements per lane.  Each wave handles one tile of 64 lanes x E elements and
 // each workgroup four tiles; launches cover the whole tensor (no grid-stride
-// loop), which measured fastest for streaming on gfx950.  Loads stay at 16 B
-// per lane where possible and each lane writes at most 32 contiguous bytes
-// (wider per-lane writes lose bandwidth).
+// loop), which measured fastest for streaming on gfx950.  Loads are 16 B per
+// lane and instruction (a quantiser lane holding more takes several 16-byte
+// chunks of its block, so each load instruction stays contiguous across the
+// block's lanes) and each lane writes at most 32 contiguous bytes (wider
+// per-lane writes lose bandwidth).  Quantiser: 4 elements per lane on fp32
+// input (8 or 16, with half or a quarter of the VALU instructions per
+// element, measured 3-5% slower), 16 on 16-bit input (2-3% faster than 8).
 #ifndef ZQ_QUANT_E_F32
 #define ZQ_QUANT_E_F32 4
 #endif
 #ifndef ZQ_QUANT_E_16
-#define ZQ_QUANT_E_16 8
+#define ZQ_QUANT_E_16 16
 #endif
 constexpr int quant_elems(int dt_bytes, int block) {
   int e = dt_bytes == 4 ? ZQ_QUANT_E_F32 : ZQ_QUANT_E_16;

@@ -263,10 +263,12 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
 }  // namespace
 
 // ------------------------------------------------------------------ quantise
-// Full blocks only.  A lane owns E consecutive elements; L = B/E lanes hold
-// one block; one wave tile is 64/L blocks; a workgroup's tiles are adjacent,
-// so thread t's codes are bytes [t*OB, (t+1)*OB) of the workgroup's output.
-// The codes and scales of a workgroup are staged in LDS and written back as
+// Full blocks only.  A lane owns E elements of one block, as C = E*size/16
+// chunks of 16 bytes: L = B/E lanes hold the block, and chunk j of the
+// block's lane i is the block's chunk j*L + i, so each load instruction of a
+// wave reads whole runs of L*16 bytes while the block's absmax, scale and
+// reciprocal are computed once per lane for all E elements.  One wave tile
+// is 64/L blocks; a workgroup's tiles are adjacent.  The codes and scales of a workgroup are staged in LDS and written back as
 // one contiguous run of 16-byte stores: at this kernel's ~8:1 read:write mix
 // that keeps the write stream from slowing the reads (per-lane 2-byte stores
 // measured ~10% slower).  A workgroup holding the last, partial tile stores
@@ -305,13 +307,17 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
                                                             uint8_t* __restrict__ out, float* __restrict__ scales,
                                                             int tail) {
   constexpr int E = quant_elems(elem_size<DT>(), B), L = B / E, BPW = 64 / L;
+  constexpr int CE = 16 / elem_size<DT>(), C = E / CE;          // elements per chunk, chunks per lane
   constexpr int T = quant_tiles(elem_size<DT>()), WAVES = kQuantThreads / 64;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
   constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane and tile
+  constexpr int OBC = OB / C;                                   // code bytes per chunk
+  constexpr int BB = B * OB / E;                                // code bytes per block
   constexpr int WG_BLOCKS = WAVES * T * BPW;                    // blocks per workgroup
   constexpr int WG_BYTES = WAVES * T * 64 * OB;                 // code bytes per workgroup
   constexpr int NWO = OB >= 4 ? OB / 4 : 1;
-  static_assert(E % 4 == 0 && L >= 1 && L <= 64 && WG_BYTES % 16 == 0, "lane layout");
+  static_assert(E % CE == 0 && L >= 1 && L <= 64 && WG_BYTES % 16 == 0, "lane layout");
+  static_assert(OBC == 2 || OBC % 4 == 0, "chunk codes");
   __shared__ u32x4 obuf[WG_BYTES / 16];
   __shared__ float sbuf[WG_BLOCKS];
 
@@ -326,15 +332,22 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   // workgroup g owns tiles [g*WAVES*T, (g+1)*WAVES*T); its t-th round of loads
   // covers WAVES adjacent tiles, one per wave
   const int64_t wg_blk0 = (int64_t)blockIdx.x * WG_BLOCKS;
+  const int li = lane % L;  // the lane's index within its block
   float v[T][E];
 #pragma unroll
   for (int t = 0; t < T; ++t) {
     const int64_t blk = wg_blk0 + (t * WAVES + wave) * BPW + lane / L;
-    if (blk < nfull) {
-      load_elems<ZQ_NT_QUANT, DT, E>(x, blk * B + (int64_t)(lane % L) * E, v[t]);
-    } else {
 #pragma unroll
-      for (int k = 0; k < E; ++k) v[t][k] = 0.0f;
+    for (int j = 0; j < C; ++j) {
+      float c[CE];
+      if (blk < nfull) {
+        load_elems<ZQ_NT_QUANT, DT, CE>(x, blk * B + (int64_t)(j * L + li) * CE, c);
+      } else {
+#pragma unroll
+        for (int k = 0; k < CE; ++k) c[k] = 0.0f;
+      }
+#pragma unroll
+      for (int k = 0; k < CE; ++k) v[t][j * CE + k] = c[k];
     }
   }
   const bool full = wg_blk0 + WG_BLOCKS <= nfull;  // workgroup-uniform
@@ -355,7 +368,8 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
 #pragma unroll
     for (int k = 0; k < E; ++k) m[k] = code_bits(v[t][k], r);
 
-    // this lane's packed codes: OB bytes, little-endian in w
+    // this lane's packed codes: OB bytes in element order (chunk j's codes are
+    // bytes [j*OBC, (j+1)*OBC)), little-endian in w
     uint32_t w[NWO];
     if constexpr (QBITS == 8) {
 #pragma unroll
@@ -367,28 +381,40 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
       for (int k = 0; k < E / 8; ++k) w[k] = pack_nibbles8(m + 8 * k);
     }
 
+    // chunk j's codes go to byte (j*L + li)*OBC of the block's codes
     if (full) {
-      char* ob = reinterpret_cast<char*>(obuf) + (slot * 64 + lane) * OB;
-      if constexpr (OB == 2) {
-        *reinterpret_cast<uint16_t*>(ob) = (uint16_t)w[0];
-      } else {
+      char* ob = reinterpret_cast<char*>(obuf) + (slot * BPW + lane / L) * BB;
 #pragma unroll
-        for (int k = 0; k < NWO; ++k) reinterpret_cast<uint32_t*>(ob)[k] = w[k];
+      for (int j = 0; j < C; ++j) {
+        char* d = ob + (j * L + li) * OBC;
+        if constexpr (OBC == 2) {
+          *reinterpret_cast<uint16_t*>(d) = (uint16_t)(w[j / 2] >> (16 * (j % 2)));
+        } else {
+#pragma unroll
+          for (int k = 0; k < OBC / 4; ++k) reinterpret_cast<uint32_t*>(d)[k] = w[j * (OBC / 4) + k];
+        }
       }
-      if (lane % L == 0) sbuf[slot * BPW + lane / L] = s;
+      if (li == 0) sbuf[slot * BPW + lane / L] = s;
     } else if (blk < nfull) {
-      uint8_t* dst = out + ((blk * B + (int64_t)(lane % L) * E) * OB) / E;
-      if constexpr (OB == 2) {
-        st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(dst), (uint16_t)w[0]);
-      } else {
-        store_words<ZQ_NT_QUANT, NWO>(dst, w);
+      uint8_t* ob = out + blk * BB;
+#pragma unroll
+      for (int j = 0; j < C; ++j) {
+        uint8_t* d = ob + (j * L + li) * OBC;
+        if constexpr (OBC == 2) {
+          st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(d), (uint16_t)(w[j / 2] >> (16 * (j % 2))));
+        } else {
+          uint32_t wc[OBC / 4];
+#pragma unroll
+          for (int k = 0; k < OBC / 4; ++k) wc[k] = w[j * (OBC / 4) + k];
+          store_words<ZQ_NT_QUANT, OBC / 4>(d, wc);
+        }
       }
-      if (lane % L == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
+      if (li == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
     }
   }
   if (full) {
     __syncthreads();
-    u32x4* dst = reinterpret_cast<u32x4*>(out + (wg_blk0 * B * OB) / E);
+    u32x4* dst = reinterpret_cast<u32x4*>(out + wg_blk0 * BB);
 #pragma unroll
     for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<ZQ_NT_QUANT>(dst + c, obuf[c]);
     if (tid < WG_BLOCKS) st<2 * ZQ_NT_SCALES>(scales + wg_blk0 + tid, sbuf[tid]);
