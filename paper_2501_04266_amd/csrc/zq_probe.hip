@@ -5,7 +5,10 @@
 // rates are the practical HBM ceilings the codec kernels are compared with.
 // Same launch style as the codec kernels: 256 threads, whole-tensor grids (no
 // grid-stride loop), 16 bytes per lane per access with consecutive lanes on
-// consecutive 16-byte chunks, nontemporal loads and stores.
+// consecutive 16-byte chunks, nontemporal loads and stores.  Chunks per
+// thread are each pattern's fastest in a sweep of 1, 2, 4 and 8 (2 GiB,
+// MI355X): copy and write one (6.5 and 6.7-6.9 TB/s, against 5.9 and 5.8
+// with four), read four (7.0-7.2 TB/s for any count).
 //
 //   zqp_copy     dst[i] = src[i]                       (1 read stream, 1 write)
 //   zqp_read     XOR of src, stored only if it equals a value the caller
@@ -25,39 +28,43 @@ namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
-constexpr int kChunks = 4;  // 16-byte chunks per thread (copy, read, write)
+constexpr int kCopyChunks = 1, kReadChunks = 4, kWriteChunks = 1;  // 16-byte chunks per thread
 
 __device__ __forceinline__ u32x4 ldnt(const u32x4* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void stnt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
-// chunk u of thread t in workgroup g: index (g * kChunks + u) * kThreads + t
+// chunk u of thread t in workgroup g: index (g * C + u) * kThreads + t, C the
+// pattern's chunks per thread
 __global__ void __launch_bounds__(kThreads) k_copy(const u32x4* __restrict__ src, u32x4* __restrict__ dst,
                                                   int64_t n16) {
-  const int64_t base = (int64_t)blockIdx.x * kChunks * kThreads + threadIdx.x;
-  u32x4 v[kChunks];
+  constexpr int C = kCopyChunks;
+  const int64_t base = (int64_t)blockIdx.x * C * kThreads + threadIdx.x;
+  u32x4 v[C];
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u)
+  for (int u = 0; u < C; ++u)
     if (base + u * kThreads < n16) v[u] = ldnt(src + base + u * kThreads);
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u)
+  for (int u = 0; u < C; ++u)
     if (base + u * kThreads < n16) stnt(dst + base + u * kThreads, v[u]);
 }
 
 __global__ void __launch_bounds__(kThreads) k_read(const u32x4* __restrict__ src, int64_t n16, u32x4* sink,
                                                   uint32_t never) {
-  const int64_t base = (int64_t)blockIdx.x * kChunks * kThreads + threadIdx.x;
+  constexpr int C = kReadChunks;
+  const int64_t base = (int64_t)blockIdx.x * C * kThreads + threadIdx.x;
   u32x4 acc = {0u, 0u, 0u, 0u};
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u)
+  for (int u = 0; u < C; ++u)
     if (base + u * kThreads < n16) acc ^= ldnt(src + base + u * kThreads);
   if (acc.x == never && acc.y == never && acc.z == never && acc.w == never) *sink = acc;
 }
 
 __global__ void __launch_bounds__(kThreads) k_write(u32x4* __restrict__ dst, int64_t n16, uint32_t pattern) {
-  const int64_t base = (int64_t)blockIdx.x * kChunks * kThreads + threadIdx.x;
+  constexpr int C = kWriteChunks;
+  const int64_t base = (int64_t)blockIdx.x * C * kThreads + threadIdx.x;
   const u32x4 v = {pattern, pattern, pattern, pattern};
 #pragma unroll
-  for (int u = 0; u < kChunks; ++u)
+  for (int u = 0; u < C; ++u)
     if (base + u * kThreads < n16) stnt(dst + base + u * kThreads, v);
 }
 
@@ -92,26 +99,26 @@ unsigned grid_of(int64_t n16, int64_t per_wg) { return (unsigned)((n16 + per_wg 
 extern "C" {
 
 int zqp_copy(const void* src, void* dst, int64_t bytes, void* stream) {
-  if (!ok16(src, bytes) || !ok16(dst, bytes) || bytes / 16 / (kChunks * kThreads) >= 0x7fffffff) return -1;
+  if (!ok16(src, bytes) || !ok16(dst, bytes) || bytes / 16 / (kCopyChunks * kThreads) >= 0x7fffffff) return -1;
   const int64_t n16 = bytes / 16;
-  hipLaunchKernelGGL(k_copy, dim3(grid_of(n16, kChunks * kThreads)), dim3(kThreads), 0,
+  hipLaunchKernelGGL(k_copy, dim3(grid_of(n16, kCopyChunks * kThreads)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(src), static_cast<u32x4*>(dst), n16);
   return status();
 }
 
 int zqp_read(const void* src, int64_t bytes, void* sink, uint32_t never, void* stream) {
-  if (!ok16(src, bytes) || !ok16(sink, 16) || bytes / 16 / (kChunks * kThreads) >= 0x7fffffff) return -1;
+  if (!ok16(src, bytes) || !ok16(sink, 16) || bytes / 16 / (kReadChunks * kThreads) >= 0x7fffffff) return -1;
   const int64_t n16 = bytes / 16;
-  hipLaunchKernelGGL(k_read, dim3(grid_of(n16, kChunks * kThreads)), dim3(kThreads), 0,
+  hipLaunchKernelGGL(k_read, dim3(grid_of(n16, kReadChunks * kThreads)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<const u32x4*>(src), n16, static_cast<u32x4*>(sink),
                      never);
   return status();
 }
 
 int zqp_write(void* dst, int64_t bytes, uint32_t pattern, void* stream) {
-  if (!ok16(dst, bytes) || bytes / 16 / (kChunks * kThreads) >= 0x7fffffff) return -1;
+  if (!ok16(dst, bytes) || bytes / 16 / (kWriteChunks * kThreads) >= 0x7fffffff) return -1;
   const int64_t n16 = bytes / 16;
-  hipLaunchKernelGGL(k_write, dim3(grid_of(n16, kChunks * kThreads)), dim3(kThreads), 0,
+  hipLaunchKernelGGL(k_write, dim3(grid_of(n16, kWriteChunks * kThreads)), dim3(kThreads), 0,
                      static_cast<hipStream_t>(stream), static_cast<u32x4*>(dst), n16, pattern);
   return status();
 }
