@@ -27,7 +27,8 @@ launches of the reduce level, and the step from 0.84 to a steady 0.75 ms
 over its first ~40 steps; the breakdown pass's events leave idle gaps that
 let the clock rise again); then the timed region of K steps, host wall clock
 between two device synchronisations, with one event pair around the
-dominant kernel only (its per-launch duration gives the roofline figure).
+dominant kernel in every fourth step only (--dom-every; its per-launch
+duration gives the roofline figure).
 All events are HIP events without the system-scope fence (TimingEvent):
 torch's default events write back and invalidate the caches when recorded
 and cost about 3 us of GPU time each, fence-free ones about 1.7 us.
@@ -847,6 +848,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--settle", type=int, default=100,
                     help="steps run after the warm-up, before timing, while the GPU's clock settles")
+    ap.add_argument("--dom-every", type=int, default=4,
+                    help="time the dominant kernel with an event pair in every N-th step of the timed region")
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the oracle timing and full check")
     ap.add_argument("--cpu-threads", type=int, default=0, help="oracle threads (default: all available)")
     ap.add_argument("--cpu-repeats", type=int, default=3, help="oracle repetitions of each timed call")
@@ -915,15 +918,17 @@ def main():
     settle = [sev[j].elapsed_time(sev[j + 1]) / nb_ for j, nb_ in enumerate(blocks)]
     log(f"settle {args.settle} steps: " + " ".join(f"{v:.3f}" for v in settle))
 
-    # timed region: K steps; the only events recorded are the pair around the
-    # dominant kernel, which gives the roofline figure
-    dev = [[TimingEvent() for _ in range(2)] for _ in range(args.steps)]
+    # timed region: K steps; the only events recorded are the pairs around the
+    # dominant kernel in every --dom-every-th step, which give the roofline
+    # figure (each pair is a barrier that costs the step a few microseconds)
+    sampled = list(range(0, args.steps, max(1, args.dom_every)))
+    dev = {k: [TimingEvent() for _ in range(2)] for k in sampled}
     r0, r1 = TimingEvent(), TimingEvent()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     r0.record()
     for k in range(args.steps):
-        L.step(dev[k], around=dom)
+        L.step(dev.get(k), around=dom)
     r1.record()
     t_enq = time.perf_counter()
     torch.cuda.synchronize()
@@ -933,7 +938,7 @@ def main():
     enqueue_ms_per_step = (t_enq - t0) * 1e3 / args.steps
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step (GPU events {gpu_ms_per_step:.3f}, "
         f"host enqueue {enqueue_ms_per_step:.3f})")
-    dom_ms = np.array([dev[k][0].elapsed_time(dev[k][1]) for k in range(args.steps)])
+    dom_ms = np.array([dev[k][0].elapsed_time(dev[k][1]) for k in sampled])
 
     step_bytes = sum(b for _, b, _ in L.calls)
     step_elems = sum(e for _, _, e in L.calls)
@@ -977,7 +982,7 @@ def main():
         "roofline": {"bound": "hbm", "kernel": dom_name, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "bytes_per_launch": dom_bytes, "us_per_launch": round(dom_ms.mean() * 1e3, 2),
-                     "us_median": round(float(np.median(dom_ms)) * 1e3, 2)},
+                     "us_median": round(float(np.median(dom_ms)) * 1e3, 2), "launches_timed": len(sampled)},
         "kernels": kernels,
     }
 
