@@ -34,8 +34,14 @@
 // Nontemporal hints per kernel family: bit 0 = loads, bit 1 = stores.  Data
 // streamed once gains from them; a kernel whose input was just written by the
 // previous call (the dequantiser after a reduce level) loses its cache hits.
-#ifndef ZQ_NT_QUANT
-#define ZQ_NT_QUANT 3
+// The quantisers: INT8 output measured faster with plain stores (the
+// degree-2 half shard 100.3 against 104.9 us), INT4 output with nontemporal
+// ones (the fp32 gradient 310.0 against 312.0 us).
+#ifndef ZQ_NT_QUANT8
+#define ZQ_NT_QUANT8 1
+#endif
+#ifndef ZQ_NT_QUANT4
+#define ZQ_NT_QUANT4 3
 #endif
 #ifndef ZQ_NT_DEQ8
 #define ZQ_NT_DEQ8 3
@@ -310,6 +316,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   constexpr int CE = 16 / elem_size<DT>(), C = E / CE;          // elements per chunk, chunks per lane
   constexpr int T = quant_tiles(elem_size<DT>()), WAVES = kQuantThreads / 64;
   constexpr float QMAX = QBITS == 8 ? 127.0f : 7.0f;
+  constexpr int NT = QBITS == 8 ? ZQ_NT_QUANT8 : ZQ_NT_QUANT4;
   constexpr int OB = QBITS == 8 ? E : E / 2;                    // code bytes per lane and tile
   constexpr int OBC = OB / C;                                   // code bytes per chunk
   constexpr int BB = B * OB / E;                                // code bytes per block
@@ -341,7 +348,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
     for (int j = 0; j < C; ++j) {
       float c[CE];
       if (blk < nfull) {
-        load_elems<ZQ_NT_QUANT, DT, CE>(x, blk * B + (int64_t)(j * L + li) * CE, c);
+        load_elems<NT, DT, CE>(x, blk * B + (int64_t)(j * L + li) * CE, c);
       } else {
 #pragma unroll
         for (int k = 0; k < CE; ++k) c[k] = 0.0f;
@@ -401,12 +408,12 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
       for (int j = 0; j < C; ++j) {
         uint8_t* d = ob + (j * L + li) * OBC;
         if constexpr (OBC == 2) {
-          st<ZQ_NT_QUANT>(reinterpret_cast<uint16_t*>(d), (uint16_t)(w[j / 2] >> (16 * (j % 2))));
+          st<NT>(reinterpret_cast<uint16_t*>(d), (uint16_t)(w[j / 2] >> (16 * (j % 2))));
         } else {
           uint32_t wc[OBC / 4];
 #pragma unroll
           for (int k = 0; k < OBC / 4; ++k) wc[k] = w[j * (OBC / 4) + k];
-          store_words<ZQ_NT_QUANT, OBC / 4>(d, wc);
+          store_words<NT, OBC / 4>(d, wc);
         }
       }
       if (li == 0) st<2 * ZQ_NT_SCALES>(scales + blk, s);
@@ -416,7 +423,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
     __syncthreads();
     u32x4* dst = reinterpret_cast<u32x4*>(out + wg_blk0 * BB);
 #pragma unroll
-    for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<ZQ_NT_QUANT>(dst + c, obuf[c]);
+    for (int c = tid; c < WG_BYTES / 16; c += kQuantThreads) st<NT>(dst + c, obuf[c]);
     if (tid < WG_BLOCKS) st<2 * ZQ_NT_SCALES>(scales + wg_blk0 + tid, sbuf[tid]);
   }
 }
