@@ -522,8 +522,9 @@ class TimingEvent:
         return ms.value
 
     def __del__(self):
+        # not at interpreter exit: the runtime may already be torn down then
         h = getattr(self, "h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and not sys.is_finalizing():
             self._hip.hipEventDestroy(h)
 
 
