@@ -129,11 +129,15 @@ int reduce(const uint8_t* packed_in, const float* scales_in, int32_t P, int64_t 
 
   // P = 2, 4, 8 on large levels: the kernel with the slice count fixed at
   // compile time (each workgroup takes reduce_fixed_tiles(P) groups)
-  ReduceKernel fixed = (ZQ_FIXED && shape != ReduceShape::kSmall) ? reduce_fixed_kernel(lgB, P, fused ? yt : -1, gather)
-                                                                  : nullptr;
+  // and on small levels (one group per workgroup, the small-level group size)
+  const bool small = shape == ReduceShape::kSmall;
+  ReduceKernel fixed = !ZQ_FIXED ? nullptr
+                       : small   ? reduce_fixed_small_kernel(lgB, P, fused ? yt : -1, gather)
+                                 : reduce_fixed_kernel(lgB, P, fused ? yt : -1, gather);
   // (its groups: the same whole-group range [0, nfull) in its own group size)
-  const int64_t fixed_groups = fixed ? nfull / (kThreads / 64 * (64 / (block / reduce_fixed_elems()))) : 0;
-  const int64_t fixed_grid = fixed ? grid_for(fixed_groups, reduce_fixed_tiles(P)) : 0;
+  const int64_t fixed_groups =
+      !fixed ? 0 : small ? groups : nfull / (kThreads / 64 * (64 / (block / reduce_fixed_elems())));
+  const int64_t fixed_grid = !fixed ? 0 : small ? groups : grid_for(fixed_groups, reduce_fixed_tiles(P));
   if (fixed && fixed_grid == 0 && groups > 0) return ZQ_E_SIZE;
 
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -107,6 +107,9 @@ ReduceGenericKernel reduce_generic_kernel(bool gather);
 // through pointer tables, INT4 output only); null where there is none.  Each
 // workgroup takes reduce_fixed_tiles(P) groups.
 ReduceKernel reduce_fixed_kernel(int lgB, int P, int ydt, bool gather);
+// The same for small levels (the small-level lane width, one group per
+// workgroup), P = 2, 4, 8; null otherwise.
+ReduceKernel reduce_fixed_small_kernel(int lgB, int P, int ydt, bool gather);
 // a chunk of 64-bit table entries passed by value to the table-fill kernel
 constexpr int kTableChunk = 64;
 struct TableChunk {

@@ -965,6 +965,9 @@ int reduce_fixed_tiles(int P) { return fixed_tiles(P); }
 #ifndef ZQ_FIXED_E
 #define ZQ_FIXED_E 32
 #endif
+#ifndef ZQ_FIXED_SMALL
+#define ZQ_FIXED_SMALL 1
+#endif
 int reduce_fixed_elems() { return ZQ_FIXED_E; }
 
 template <int B, int YDT, bool GATHER>
@@ -990,6 +993,33 @@ ReduceKernel reduce_fixed_kernel(int lgB, int P, int ydt, bool gather) {
     case ZQ_F16: return reduce_fixed_for<ZQ_F16, false>(lgB, P);
     case ZQ_BF16: return reduce_fixed_for<ZQ_BF16, false>(lgB, P);
     default: return reduce_fixed_for<-1, false>(lgB, P);
+  }
+}
+
+// Small levels (E = 8, the small-level group size): P = 2, 4, 8 fixed at
+// compile time, one group per workgroup.
+template <int B, int YDT, bool GATHER>
+static ReduceKernel reduce_fixed_small_for_b(int P) {
+  if (P == 2) return &k_reduce_p<B, 8, 2, 1, YDT, GATHER>;
+  if (P == 4) return &k_reduce_p<B, 8, 4, 1, YDT, GATHER>;
+  return &k_reduce_p<B, 8, 8, 1, YDT, GATHER>;
+}
+
+template <int YDT, bool GATHER>
+static ReduceKernel reduce_fixed_small_for(int lgB, int P) {
+  if (lgB == 6) return reduce_fixed_small_for_b<64, YDT, GATHER>(P);
+  if (lgB == 7) return reduce_fixed_small_for_b<128, YDT, GATHER>(P);
+  return reduce_fixed_small_for_b<256, YDT, GATHER>(P);
+}
+
+ReduceKernel reduce_fixed_small_kernel(int lgB, int P, int ydt, bool gather) {
+  if (!ZQ_FIXED_SMALL || lgB < 6 || lgB > 8 || (P != 2 && P != 4 && P != 8) || (gather && ydt >= 0)) return nullptr;
+  if (gather) return reduce_fixed_small_for<-1, true>(lgB, P);
+  switch (ydt) {
+    case ZQ_F32: return reduce_fixed_small_for<ZQ_F32, false>(lgB, P);
+    case ZQ_F16: return reduce_fixed_small_for<ZQ_F16, false>(lgB, P);
+    case ZQ_BF16: return reduce_fixed_small_for<ZQ_BF16, false>(lgB, P);
+    default: return reduce_fixed_small_for<-1, false>(lgB, P);
   }
 }
 

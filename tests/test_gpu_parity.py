@@ -440,6 +440,12 @@ SPECIAL_REDUCE_CASES = [
     ("huge", 3, 128, (1 << 23) + 4096),
     ("huge", 3, 256, 65536 + 256),
     ("huge", 2, 64, 1000),
+    # small levels with the slice count fixed at compile time (P = 2, 4, 8)
+    ("huge", 2, 128, 65536 + 128),
+    ("huge", 4, 64, 32768),
+    ("huge", 8, 256, 65536 + 256),
+    ("subthreshold", 4, 256, 65536 + 256),
+    ("subthreshold", 2, 64, 2048 * 3 + 64),
 ]
 
 
@@ -477,14 +483,19 @@ def test_reduce_edge_sums(kind, P, block, m):
     assert_bits_equal(from_dev(hs), so, f"{what} gather scales")
 
 
-# The compile-time-P kernel (P = 2, 4, 8; B = 64, 128, 256) at sizes where its
-# workgroups take T = 4 groups (P = 2) and the group count leaves 1, 2 or 3
-# over, so the last workgroup clamps to the last group and recomputes it;
-# some sizes also leave a block for the generic kernel.  Plain, fused (f32,
-# bf16) and gathered.
+# The compile-time-P kernels (P = 2, 4, 8; B = 64, 128, 256): on large levels
+# at sizes where the workgroups take T = 4 groups (P = 2) and the group count
+# leaves 1, 2 or 3 over, so the last workgroup clamps to the last group and
+# recomputes it; on small levels (8 elements per lane, one group per
+# workgroup) from one group up.  Some sizes also leave a block for the
+# generic kernel.  Plain, fused (f32, bf16) and gathered.
 FIXED_P_CASES = [(2, 128, 8192 * 4097), (2, 128, 8192 * 4098 + 128), (2, 256, 8192 * 4099),
                  (2, 64, 8192 * 4097 + 64), (4, 64, 8192 * 4098), (4, 256, 8192 * 4099),
-                 (8, 64, 8192 * 4098), (8, 256, 8192 * 4097)]
+                 (8, 64, 8192 * 4098), (8, 256, 8192 * 4097),
+                 # small levels: groups of 2,048 elements, one per workgroup
+                 (2, 64, 2048 * 5 + 64), (2, 128, 2048), (2, 256, 2048 * 33 + 512),
+                 (4, 64, 2048 * 7), (4, 128, 2048 * 100 + 128), (4, 256, 2048 * 3 + 256),
+                 (8, 64, 2048 * 9 + 64), (8, 128, 2048 * 64), (8, 256, 2048 * 11 + 256)]
 
 
 def _random_level(P, m, block, seed):
