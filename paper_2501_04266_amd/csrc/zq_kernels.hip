@@ -274,8 +274,9 @@ __device__ __forceinline__ void store1(void* p, int64_t i, float v) {
 // block's lane i is the block's chunk j*L + i, so each load instruction of a
 // wave reads whole runs of L*16 bytes while the block's absmax, scale and
 // reciprocal are computed once per lane for all E elements.  One wave tile
-// is 64/L blocks; a workgroup's tiles are adjacent.  The codes and scales of a workgroup are staged in LDS and written back as
-// one contiguous run of 16-byte stores: at this kernel's ~8:1 read:write mix
+// is 64/L blocks; a workgroup's tiles are adjacent.  The codes and scales of
+// a workgroup are staged in LDS and written back as one contiguous run of
+// 16-byte stores: at this kernel's ~8:1 read:write mix
 // that keeps the write stream from slowing the reads (per-lane 2-byte stores
 // measured ~10% slower).  A workgroup holding the last, partial tile stores
 // straight from its lanes instead.  When n is not a multiple of B, one more
@@ -708,8 +709,9 @@ __global__ void __launch_bounds__(kThreads) k_reduce(const uint8_t* __restrict__
   }
 }
 
-// Vector path with the slice count fixed at compile time (PC = 2, 4 or 8).
-// Same lane layout, arithmetic and order as k_reduce, but every load is
+// Vector path with the slice count fixed at compile time (PC = 2, 4 or 8;
+// E = 32 on large levels, E = 8 on small ones).  Same lane layout,
+// arithmetic and order as k_reduce, but every load is
 // unconditional, so the compiler waits for each slice's data on its own
 // (s_waitcnt vmcnt(n) counting the loads issued after it) instead of for
 // every load in flight, and the sum of slice 0 starts while the others are
