@@ -37,6 +37,26 @@
 // The quantisers: INT8 output measured faster with plain stores (the
 // degree-2 half shard 100.3 against 104.9 us), INT4 output with nontemporal
 // ones (the fp32 gradient 310.0 against 312.0 us).
+// Wave priority while a wave issues its loads (s_setprio, within the
+// kernel): raised so that the loads of a newly started wave go out ahead of
+// other waves' arithmetic, then back to normal for the wave's own arithmetic.
+#ifndef ZQ_PRIO_QUANT
+#define ZQ_PRIO_QUANT 1
+#endif
+#ifndef ZQ_PRIO_REDUCE
+#define ZQ_PRIO_REDUCE 0
+#endif
+#ifndef ZQ_PRIO_DEQ
+#define ZQ_PRIO_DEQ 0
+#endif
+template <int ON>
+__device__ __forceinline__ void prio_issue() {
+  if constexpr (ON) __builtin_amdgcn_s_setprio(3);
+}
+template <int ON>
+__device__ __forceinline__ void prio_compute() {
+  if constexpr (ON) __builtin_amdgcn_s_setprio(0);
+}
 #ifndef ZQ_NT_QUANT8
 #define ZQ_NT_QUANT8 1
 #endif
@@ -341,6 +361,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
   // covers WAVES adjacent tiles, one per wave
   const int64_t wg_blk0 = (int64_t)blockIdx.x * WG_BLOCKS;
   const int li = lane % L;  // the lane's index within its block
+  prio_issue<ZQ_PRIO_QUANT>();
   float v[T][E];
 #pragma unroll
   for (int t = 0; t < T; ++t) {
@@ -358,6 +379,7 @@ __global__ void __launch_bounds__(kQuantThreads) k_quantize(const void* __restri
       for (int k = 0; k < CE; ++k) v[t][j * CE + k] = c[k];
     }
   }
+  prio_compute<ZQ_PRIO_QUANT>();
   const bool full = wg_blk0 + WG_BLOCKS <= nfull;  // workgroup-uniform
 #pragma unroll
   for (int t = 0; t < T; ++t) {
@@ -456,8 +478,10 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
   if (STAGE && g0 + kDeqThreads <= ngroups) {  // workgroup-uniform
     const int64_t e0 = gid * E;
     uint32_t w[IB / 4];
+    prio_issue<ZQ_PRIO_DEQ>();
     load_words<NT, IB / 4>(codes + (e0 * IB) / E, w);
     const float s = ld<NT>(scales + (e0 >> lgB));
+    prio_compute<ZQ_PRIO_DEQ>();
     float v[E];
 #pragma unroll
     for (int k = 0; k < E; ++k) {
@@ -472,8 +496,10 @@ __global__ void __launch_bounds__(kDeqThreads) k_dequant(const uint8_t* __restri
   } else if (gid < ngroups) {
     const int64_t e0 = gid * E;
     uint32_t w[IB / 4];
+    prio_issue<ZQ_PRIO_DEQ>();
     load_words<NT, IB / 4>(codes + (e0 * IB) / E, w);
     const float s = ld<NT>(scales + (e0 >> lgB));
+    prio_compute<ZQ_PRIO_DEQ>();
     float v[E];
 #pragma unroll
     for (int k = 0; k < E; ++k) {
@@ -765,10 +791,16 @@ __global__ void __launch_bounds__(kThreads) ZQ_FIXED_ATTR k_reduce_p(const uint8
     }
   };
 
+  prio_issue<ZQ_PRIO_REDUCE>();
   issue(0, group_of(0));
+  prio_compute<ZQ_PRIO_REDUCE>();
 #pragma unroll
   for (int t = 0; t < TRC; ++t) {
-    if (t + 1 < TRC) issue((t + 1) % NBUF, group_of(t + 1));
+    if (t + 1 < TRC) {
+      prio_issue<ZQ_PRIO_REDUCE>();
+      issue((t + 1) % NBUF, group_of(t + 1));
+      prio_compute<ZQ_PRIO_REDUCE>();
+    }
     const int b = t % NBUF;
     float acc[E];
     add_slice<E, NW, true>(acc, w[b][0], sc[b][0]);
