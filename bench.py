@@ -602,7 +602,7 @@ def load_trace(call):
 
 class Probe:
     """The bandwidth-ceiling kernels of libzq_probe.so (copy, read, write,
-    P read streams + one write stream)."""
+    P read streams + one write stream, 8 bytes in + 16 out per thread)."""
 
     def __init__(self):
         import ctypes
@@ -614,7 +614,8 @@ class Probe:
         L = ctypes.CDLL(zbuild.PROBE_LIB)
         vp, i64, i32, u32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_uint32
         for name, args in {"zqp_copy": [vp, vp, i64, vp], "zqp_read": [vp, i64, vp, u32, vp],
-                           "zqp_write": [vp, i64, u32, vp], "zqp_streams": [vp, i32, i64, vp, vp]}.items():
+                           "zqp_write": [vp, i64, u32, vp], "zqp_streams": [vp, i32, i64, vp, vp],
+                           "zqp_expand": [vp, i64, vp, vp]}.items():
             getattr(L, name).argtypes, getattr(L, name).restype = args, ctypes.c_int
         self.L, self.torch = L, torch
 
@@ -660,6 +661,10 @@ class Probe:
             key = f"P={P} m={m}"
             streams[key] = {"GBps": round(fp / (us * 1e-6) / 1e9, 1), "us": round(us, 2), "rotated_sets": nsets}
         res["reduce_pattern"] = streams
+        # the INT8 -> 16-bit dequantiser's pattern at the layer's size: n bytes
+        # in, 2n out, 8 bytes loaded and 16 stored per thread
+        us = loop_us([lambda: self._ok(L.zqp_expand(A, n, B_, self._st()), "expand")], reps)
+        res["dequant_pattern"] = {"n": n, "GBps": round(3 * n / (us * 1e-6) / 1e9, 1), "us": round(us, 2)}
         del a, b
         T.cuda.empty_cache()
         return res

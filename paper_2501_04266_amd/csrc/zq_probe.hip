@@ -17,6 +17,9 @@
 //   zqp_streams  dst[i] = XOR over p of src[p * slice + i]: the reduce level's
 //                pattern (P read streams of slice_bytes, back to back, and one
 //                write stream of slice_bytes)
+//   zqp_expand   each thread loads 8 bytes and stores 16: the INT8 -> 16-bit
+//                dequantiser's pattern (one read stream, a write stream twice
+//                its size)
 //
 // Sizes are bytes and must be multiples of 16; pointers 16-byte aligned.
 // Every call returns 0, or -1 on a bad argument (checked before any launch),
@@ -27,10 +30,12 @@
 namespace {
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kThreads = 256;
 constexpr int kCopyChunks = 1, kReadChunks = 4, kWriteChunks = 1;  // 16-byte chunks per thread
 
 __device__ __forceinline__ u32x4 ldnt(const u32x4* p) { return __builtin_nontemporal_load(p); }
+__device__ __forceinline__ u32x2 ldnt(const u32x2* p) { return __builtin_nontemporal_load(p); }
 __device__ __forceinline__ void stnt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
 
 // chunk u of thread t in workgroup g: index (g * C + u) * kThreads + t, C the
@@ -86,6 +91,16 @@ __global__ void __launch_bounds__(kThreads) k_streams(const u32x4* __restrict__ 
   stnt(dst + i, acc);
 }
 
+// thread i: 8 bytes in at i, 16 bytes out at i (the dequantiser's one tile
+// per wave, each store instruction covering 1 KiB)
+__global__ void __launch_bounds__(kThreads) k_expand(const u32x2* __restrict__ src, int64_t n8,
+                                                    u32x4* __restrict__ dst) {
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n8) return;
+  const u32x2 v = ldnt(src + i);
+  stnt(dst + i, u32x4{v.x ^ 0x55555555u, v.x, v.y ^ 0x33333333u, v.y});
+}
+
 bool ok16(const void* p, int64_t bytes) {
   return p != nullptr && (reinterpret_cast<uintptr_t>(p) & 15) == 0 && bytes > 0 && bytes % 16 == 0;
 }
@@ -130,6 +145,14 @@ int zqp_streams(const void* src, int32_t P, int64_t slice_bytes, void* dst, void
   const int64_t slice16 = slice_bytes / 16;
   hipLaunchKernelGGL(k_streams, dim3(grid_of(slice16, kThreads)), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
                      static_cast<const u32x4*>(src), (int)P, slice16, static_cast<u32x4*>(dst));
+  return status();
+}
+
+int zqp_expand(const void* src, int64_t in_bytes, void* dst, void* stream) {
+  if (!ok16(src, in_bytes) || !ok16(dst, 2 * in_bytes) || in_bytes / 8 / kThreads >= 0x7fffffff) return -1;
+  const int64_t n8 = in_bytes / 8;
+  hipLaunchKernelGGL(k_expand, dim3(grid_of(n8, kThreads)), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+                     static_cast<const u32x2*>(src), n8, static_cast<u32x4*>(dst));
   return status();
 }
 
