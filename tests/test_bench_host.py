@@ -117,3 +117,16 @@ def test_timing_event_binds_the_hip_runtime_torch_loaded():
     maps = [ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64.so" in ln]
     assert maps and hip._name == maps[0]
     assert bench.HIP_EVENT_DISABLE_SYSTEM_FENCE == 0x20000000
+
+
+def test_ceiling_library_exports_what_the_bench_binds():
+    # symbols only: loading the library launches nothing
+    import ctypes
+
+    from paper_2501_04266_amd import build as zbuild
+    if not os.path.exists(zbuild.PROBE_LIB):
+        import pytest
+        pytest.skip("libzq_probe.so is not built")
+    lib = ctypes.CDLL(zbuild.PROBE_LIB)
+    for name in ("zqp_copy", "zqp_read", "zqp_write", "zqp_streams", "zqp_expand"):
+        assert hasattr(lib, name), name
