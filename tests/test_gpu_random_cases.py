@@ -2,7 +2,7 @@
 from 1 to ~3e5 elements, every block size, dtype and output type, P up to
 64), each case bit for bit against the oracle.  Complements the hand-picked
 edge cases with combinations nobody chose.  ZQ_RANDOM_CASES sets the count
-(default 120)."""
+(default 120), ZQ_RANDOM_SEED the seed of the case draws (default 2025)."""
 import os
 
 import numpy as np
@@ -34,7 +34,10 @@ def _x(g, n, dt):
     return x
 
 
-def _cases(count=int(os.environ.get("ZQ_RANDOM_CASES", "120")), seed=2025):
+SEED = int(os.environ.get("ZQ_RANDOM_SEED", "2025"))
+
+
+def _cases(count=int(os.environ.get("ZQ_RANDOM_CASES", "120")), seed=SEED):
     g = np.random.default_rng(seed)
     out = []
     for i in range(count):
@@ -46,7 +49,7 @@ def _cases(count=int(os.environ.get("ZQ_RANDOM_CASES", "120")), seed=2025):
 
 @pytest.mark.parametrize("i,op,n,block,dt,out,P", _cases())
 def test_random_case(i, op, n, block, dt, out, P):
-    g = np.random.default_rng(10_000 + i)
+    g = np.random.default_rng(10_000 + i if SEED == 2025 else [SEED, i])
     what = f"case {i}: {op} n={n} B={block} in={dt} out={out} P={P}"
     if op in ("qwz", "qgz"):
         x = _x(g, n, dt)
